@@ -1,0 +1,280 @@
+"""ReTopK decode-step benchmark on one MI355X.
+
+One step = one ReTopK decode step over every query head of the layer (the whole
+hot path: similarity recall, path rule, candidate union, candidate or
+full-history scoring, Top-K, Softmax-V, cache insert).  The default workload is
+the 128K-context layer: 32 query / 8 KV heads, d = 128, bf16, K = 512, cache
+capacity 512, r = 8, W = 256, tau = 0.8, refresh period 64, 256 decode steps, on
+synthetic clustered keys and query walks (paper_2607_27692_amd/inputs.py).
+
+Timing: inputs are resident in HBM before timing starts.  Prefill
+initialisation is untimed.  Each timed step is bracketed by HIP events on the
+launch stream; between steps a 1 GiB buffer is rewritten (outside the events) so
+that every step starts with cold L2 and MALL caches, as it would between two
+layers of a model.  The Exact Top-K baseline (exact_topk_attention) runs over
+the same queries and lengths under the same protocol.  Kernel durations come
+from the library's own event profiling over the timed steps.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+METRIC = "µs per decode step (all heads) + speedup vs Exact Top-K, 128K ctx, K=512"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", default="128k")
+    ap.add_argument("--warm", action="store_true", help="no cache flush between steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--profile-kernels", type=int, default=1)
+    return ap.parse_args()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); the "
+              "multi-GPU layout is a design note only", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2607_27692_amd import retopk as R
+    from paper_2607_27692_amd.inputs import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    K_steps = min(args.steps, w.steps)
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    inp = make_inputs(w)
+    log(f"[bench] inputs {w.name} generated in {time.time() - t0:.1f}s")
+
+    def dev(raw):
+        if raw.dtype == np.uint16:
+            return torch.from_numpy(raw.view(np.int16)).to("cuda")
+        return torch.from_numpy(raw).to("cuda")
+
+    q_tail, q_dec, k, v = (dev(inp.q_tail_raw), dev(inp.q_dec_raw), dev(inp.k_raw),
+                           dev(inp.v_raw))
+    cfg = dict(batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+               head_dim=w.head_dim, max_len=w.max_len, k=w.k, cache_cap=w.cache_cap, r=w.r,
+               window=w.window, tau=w.tau, refresh=w.refresh, dtype=w.dtype)
+    out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    sel = torch.empty((w.batch, w.n_q_heads, w.k), dtype=torch.int32, device="cuda")
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
+    stream = torch.cuda.current_stream()
+
+    def fresh_handle():
+        h = R.Handle(**cfg)
+        h.prefill_init(q_tail, w.cache_cap, k, v, w.prompt_len)
+        return h
+
+    # ---- warm-up (separate handle, then discarded) --------------------------
+    h = fresh_handle()
+    for t in range(min(args.warmup, w.steps)):
+        h.decode_step(q_dec[t], k, v, w.step_len(t), out, sel)
+        h.exact(q_dec[t], k, v, w.step_len(t), out, sel)
+    torch.cuda.synchronize()
+    h.close()
+    log("[bench] warm-up done")
+
+    def timed(run, handle):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K_steps)]
+        handle.profile(bool(args.profile_kernels))
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        for t in range(K_steps):
+            if not args.warm:
+                flush.fill_(float(t))
+            ev[t][0].record(stream)
+            run(handle, t)
+            ev[t][1].record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        prof = handle.profile_read() if args.profile_kernels else {}
+        handle.profile(False)
+        ms = np.array([a.elapsed_time(b) for a, b in ev])
+        return ms, wall, prof
+
+    # ---- ReTopK ---------------------------------------------------------------
+    h = fresh_handle()
+    st0 = h.stats()
+    r_ms, r_wall, r_prof = timed(
+        lambda hh, t: hh.decode_step(q_dec[t], k, v, w.step_len(t), out, sel), h)
+    st = h.stats()
+    h.close()
+    log(f"[bench] ReTopK: {r_ms.mean() * 1e3:.1f} us/step (median {np.median(r_ms) * 1e3:.1f})")
+
+    # ---- Exact Top-K baseline -------------------------------------------------
+    h = fresh_handle()
+    e_ms, e_wall, e_prof = timed(
+        lambda hh, t: hh.exact(q_dec[t], k, v, w.step_len(t), out, sel), h)
+    h.close()
+    log(f"[bench] Exact: {e_ms.mean() * 1e3:.1f} us/step (median {np.median(e_ms) * 1e3:.1f})")
+
+    # ---- algorithmic bytes ------------------------------------------------------
+    e = 2 if w.dtype == "bf16" else 4
+    d = w.head_dim
+    lens = np.array([w.step_len(t) for t in range(K_steps)], np.float64)
+    BH = w.batch * w.n_q_heads
+    head_steps = st["head_steps"] - st0["head_steps"]
+    reuse = st["reuse"] - st0["reuse"]
+    fallback = st["fallback"] - st0["fallback"]
+    refresh = st["refresh"] - st0["refresh"]
+    scans = st["kv_group_scans"] - st0["kv_group_scans"]
+    cand_sum = st["cand_sum"] - st0["cand_sum"]
+    exact_heads = head_steps - reuse
+    mean_len = lens.mean()
+    # Per step: q, V rows of the support, output, cache insert for every head;
+    # cached queries and supports read on reuse; key rows scanned or gathered.
+    C_valid = w.cache_cap
+    per_head_fixed = d * e + w.k * d * e + d * 4 + d * 4 + w.k * 4
+    retopk_bytes = (head_steps * per_head_fixed
+                    + (reuse + fallback) * C_valid * d * 4
+                    + reuse * w.r * w.k * 4
+                    + cand_sum * d * e
+                    + scans * mean_len * d * e)
+    exact_bytes = K_steps * (w.batch * w.n_kv_heads * mean_len * d * e
+                             + BH * (w.k * d * e + d * e + d * 4))
+    r_us, e_us = r_ms.mean() * 1e3, e_ms.mean() * 1e3
+    step_gbs = retopk_bytes / K_steps / (r_us * 1e-6) / 1e9
+    exact_gbs = exact_bytes / K_steps / (e_us * 1e-6) / 1e9
+
+    # Dominant kernel of the ReTopK step and its algorithmic bytes per launch.
+    roof = None
+    if r_prof:
+        dom = max(r_prof, key=lambda n: r_prof[n][1])
+        launches, tot_ms = r_prof[dom]
+        if dom == "retopk_score":
+            kbytes = scans * mean_len * d * e + cand_sum * d * e + reuse * d * e
+        elif dom == "retopk_select":
+            kbytes = (reuse + fallback) * (C_valid * d * 4 + d * e) + reuse * w.r * w.k * 4
+        else:
+            kbytes = exact_heads * (mean_len * 4 + w.k * d * e + d * 4)
+        ach = kbytes / launches / (tot_ms / launches * 1e-3) / 1e9
+        roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                "traffic": None,
+                "avg_launch_us": round(tot_ms / launches * 1e3, 2), "launches": launches,
+                "bytes_per_launch": round(kbytes / launches)}
+    exact_roof = None
+    if e_prof and "retopk_score" in e_prof:
+        launches, tot_ms = e_prof["retopk_score"]
+        scan_bytes = K_steps * w.batch * w.n_kv_heads * mean_len * d * e
+        ach = scan_bytes / (tot_ms * 1e-3) / 1e9
+        exact_roof = {"kernel": "retopk_score (full scan)", "achieved": round(ach, 1),
+                      "frac": round(ach / HBM_PEAK_GBS, 4),
+                      "avg_launch_us": round(tot_ms / launches * 1e3, 2)}
+
+    # ---- CPU baseline: the oracle on a bounded sample ------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, inp, args.cpu_seconds)
+
+    res = {
+        "metric": METRIC,
+        "value": round(r_us, 2),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": K_steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r_us / 1e3, 5),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "q_heads": w.n_q_heads,
+                   "kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "context": w.prompt_len, "k": w.k, "cache_cap": w.cache_cap, "r": w.r,
+                   "window": w.window, "tau": w.tau, "refresh": w.refresh,
+                   "cache_state": "warm" if args.warm else "cold (1 GiB flush between steps)"},
+        "speedup_vs_exact": round(e_us / r_us, 3),
+        "exact_us_per_step": round(e_us, 2),
+        "retopk_us_median": round(float(np.median(r_ms)) * 1e3, 2),
+        "exact_us_median": round(float(np.median(e_ms)) * 1e3, 2),
+        "fallback_rate": round(fallback / head_steps, 4) if head_steps else None,
+        "refresh_share": round(refresh / head_steps, 4) if head_steps else None,
+        "mean_candidates": round(cand_sum / reuse, 1) if reuse else None,
+        "max_candidates": st["cand_max"],
+        "kv_group_scans_per_step": round(scans / K_steps, 3),
+        "step_hbm_gbs": round(step_gbs, 1),
+        "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
+        "exact_hbm_gbs": round(exact_gbs, 1),
+        "exact_hbm_frac": round(exact_gbs / HBM_PEAK_GBS, 4),
+        "wall_s_timed": round(r_wall, 4),
+        "kernels_retopk": {n: {"launches": l, "avg_us": round(ms / l * 1e3, 2) if l else None}
+                           for n, (l, ms) in r_prof.items()},
+        "kernels_exact": {n: {"launches": l, "avg_us": round(ms / l * 1e3, 2) if l else None}
+                          for n, (l, ms) in e_prof.items()},
+        "roofline": roof,
+        "exact_roofline": exact_roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+def cpu_baseline(w, inp, seconds: float):
+    """The oracle, single-threaded, on KV group 0's query heads: Exact Top-K steps,
+    then ReTopK decode steps from a seeded cache state, until about `seconds` of
+    CPU time is spent; scaled to all heads of the layer."""
+    from oracle import oracle as O
+    from paper_2607_27692_amd.inputs import make_support_state
+
+    G = w.group
+    heads = list(range(G))
+    mask = np.zeros(w.batch * w.n_q_heads, np.uint8)
+    mask[heads] = 1
+    p = O.Params(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_len, w.k, w.cache_cap,
+                 w.r, w.window, w.tau, w.refresh)
+    kf, vf = inp.k, inp.v
+    t0 = time.process_time()
+    n_ex = 0
+    while n_ex < 2 or (time.process_time() - t0 < seconds / 2 and n_ex < w.steps):
+        O.exact(p, inp.q_dec[n_ex], kf, vf, w.step_len(n_ex), head_mask=mask)
+        n_ex += 1
+    ex_s = (time.process_time() - t0) / n_ex
+    supp, cnt = make_support_state(inp, heads=heads)
+    qbar = np.zeros((w.batch * w.n_q_heads, w.cache_cap, w.head_dim), np.float32)
+    for hh in heads:
+        qbar[hh] = np.stack([O.normalize(inp.q_tail[0, hh, u]) for u in range(w.cache_cap)])
+    orc = O.Oracle(p)
+    orc.set_state(qbar, supp, cnt, w.cache_cap, 1)
+    t1 = time.process_time()
+    n_st = 0
+    while n_st < 2 or (time.process_time() - t1 < seconds / 2 and n_st < w.steps):
+        orc.decode_step(inp.q_dec[n_st], kf, vf, w.step_len(n_st), head_mask=mask)
+        n_st += 1
+    st_s = (time.process_time() - t1) / n_st
+    scale = (w.batch * w.n_q_heads) / len(heads)
+    return {"value": round(st_s * scale * 1e6, 1), "unit": "us/step", "cores": 1,
+            "kind": "oracle",
+            "exact_us_per_step": round(ex_s * scale * 1e6, 1),
+            "sample": (f"oracle (plain C, 1 thread) on the {len(heads)} query heads of KV group "
+                       f"0, {n_st} ReTopK steps from a seeded cache state and {n_ex} Exact "
+                       f"Top-K steps, scaled x{scale:g} to all heads"),
+            "cpu": platform.processor() or platform.machine()}
+
+
+if __name__ == "__main__":
+    main()

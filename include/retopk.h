@@ -1,0 +1,170 @@
+/*
+ * retopk.h -- C ABI of the MI355X (gfx950) ReTopK decode-step library.
+ *
+ * ReTopK ("Recall Before You Rank: Similarity-Guided Top-K Reuse for Efficient
+ * Long-Context Attention") replaces the full-history Exact Top-K selection of
+ * sparse decode attention (Eq. 1, Eq. 4) by a recall-before-rerank step
+ * (Sec. 3.3): the current query is matched against a bounded per-head cache of
+ * normalised past queries (Eq. 5, Eq. 6), the supports of the R most similar
+ * entries are united with a recent window (Eq. 7-9), only that candidate set is
+ * scored with the current query (Eq. 10) and reranked to K entries (Eq. 11), and
+ * Softmax-V runs over those K rows (Eq. 12).  When the best similarity is below
+ * tau, or every T_r decode steps, the step falls back to Exact Top-K instead
+ * (Eq. 13, Sec. 3.4).  Either way (q_bar, support) is inserted into the cache.
+ *
+ * Tensor layouts (all row-major, device memory unless stated):
+ *   q        [B, Hq, d]            current queries, element type = config dtype
+ *   q_tail   [B, Hq, n, d]         prompt-tail queries for retopk_prefill_init
+ *   k, v     [B, Hkv, max_len, d]  complete KV cache; rows [0, len) are valid
+ *   out      [B, Hq, d]            float32 attention output
+ *   sel      [B, Hq, K]            int32 selected support, ascending, -1 padded
+ * Query head h uses KV head h / (Hq / Hkv).  The caller owns every pointer it
+ * passes; the library owns the per-head caches and all workspaces, allocated in
+ * retopk_create and released in retopk_destroy.  No step call allocates memory.
+ *
+ * Streams: the step calls are asynchronous on the HIP stream passed in
+ * (a hipStream_t, NULL = the null stream); path decisions stay on the device.
+ * retopk_stats, retopk_get_state, retopk_set_state and retopk_profile_read
+ * synchronise the stream of the last step call.  A handle is not thread-safe
+ * and its step calls must not overlap.
+ *
+ * Errors: arguments are checked on the host before any device work; a failing
+ * check returns RETOPK_ERR_ARG (or RETOPK_ERR_UNSUPPORTED for a shape the
+ * kernels are not built for) and changes nothing.  A HIP failure returns
+ * RETOPK_ERR_HIP and marks the handle broken: later step calls return
+ * RETOPK_ERR_STATE.
+ */
+#ifndef RETOPK_H
+#define RETOPK_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct retopk_handle_s *retopk_handle;
+
+typedef enum { RETOPK_F32 = 0, RETOPK_BF16 = 1 } retopk_dtype;
+
+typedef enum {
+    RETOPK_OK = 0,
+    RETOPK_ERR_ARG = -1,          /* invalid argument or null pointer          */
+    RETOPK_ERR_UNSUPPORTED = -2,  /* valid, but no kernel for this shape        */
+    RETOPK_ERR_OOM = -3,          /* device allocation failed in retopk_create  */
+    RETOPK_ERR_HIP = -4,          /* a HIP runtime call failed                  */
+    RETOPK_ERR_STATE = -5         /* call out of order (see each function)      */
+} retopk_status;
+
+/* Path taken by one (sequence, query head) in one step (Eq. 13). */
+typedef enum {
+    RETOPK_REUSE = 0,     /* recall-before-rerank (Sec. 3.3)                    */
+    RETOPK_FALLBACK = 1,  /* rho_max < tau: Exact Top-K (Sec. 3.4)              */
+    RETOPK_REFRESH = 2,   /* scheduled refresh, t_dec in {T_r, 2T_r, ...}       */
+    RETOPK_COLD = 3       /* the cache is empty (capacity 0 or nothing inserted)*/
+} retopk_path;
+
+typedef struct {
+    int32_t batch;       /* B >= 1                                               */
+    int32_t n_q_heads;   /* Hq >= 1                                              */
+    int32_t n_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0, Hq / Hkv in {1, 2, 4, 8}    */
+    int32_t head_dim;    /* d in {64, 128}                                       */
+    int64_t max_len;     /* rows allocated per (b, KV head) in k and v, < 2^31   */
+    int32_t k;           /* K: support size, 1 <= K <= 2048                      */
+    int32_t cache_cap;   /* C (paper), M: cache entries per query head, 0..4096  */
+    int32_t r;           /* R (paper): retrieved entries per step, 1..32         */
+    int32_t window;      /* W: recent window, >= 0                               */
+    float   tau;         /* fallback threshold on rho_max, finite                */
+    int32_t refresh;     /* T_r (paper), P: refresh period in steps, 0 = off     */
+    int32_t dtype;       /* retopk_dtype of q, k and v                           */
+} retopk_config;
+
+/* Cumulative counters since retopk_create (or the last retopk_set_state). */
+typedef struct {
+    uint64_t steps;           /* retopk_decode_step calls                        */
+    uint64_t head_steps;      /* steps x B x Hq                                  */
+    uint64_t reuse;           /* head-steps per path                             */
+    uint64_t fallback;
+    uint64_t refresh;
+    uint64_t cold;
+    uint64_t kv_group_scans;  /* (b, KV head) full-history scans run             */
+    uint64_t cand_sum;        /* sum of |candidate set| over reuse head-steps    */
+    uint64_t cand_max;        /* largest |candidate set|                         */
+} retopk_stats_t;
+
+/* Optional per-step diagnostics of retopk_decode_step (device pointers, each may
+ * be NULL).  Slots are cache positions: the i-th insertion goes to slot i mod C. */
+typedef struct {
+    int8_t  *path;       /* [B*Hq] retopk_path                                  */
+    double  *rho_max;    /* [B*Hq] best cosine similarity; NaN when not computed */
+    int32_t *retrieved;  /* [B*Hq*r] retrieved slots, best first, -1 padded     */
+    int32_t *n_cand;     /* [B*Hq] |candidate set| on reuse, else 0             */
+    int32_t *cand;       /* [B*Hq*(r*K+W)] candidate set ascending, -1 padded   */
+} retopk_debug;
+
+/* Create a handle: validates cfg and allocates the caches (C entries of d floats
+ * and K indices per query head, Eq. 5, metadata cost of Sec. 3.5) and the step
+ * workspaces on the current HIP device.  The cache starts empty. */
+retopk_status retopk_create(const retopk_config *cfg, retopk_handle *out);
+
+/* Release everything retopk_create allocated.  NULL is accepted. */
+retopk_status retopk_destroy(retopk_handle h);
+
+/* Cache initialisation from the prompt tail (Sec. 3.3): q_tail holds the queries
+ * at positions prefill_len-n .. prefill_len-1; query u is given its Exact Top-K
+ * support over its causal prefix (len = prefill_len-n+u+1) and inserted, in
+ * order.  Requires n >= 0 and n <= prefill_len <= max_len.  Does not advance the
+ * decode-step counter. */
+retopk_status retopk_prefill_init(retopk_handle h, const void *q_tail, int32_t n,
+                                  const void *k, const void *v, int64_t prefill_len,
+                                  void *stream);
+
+/* One ReTopK decode step for every (sequence, query head) over KV rows [0, len)
+ * (Sec. 3.3-3.4).  The path is chosen per head on the device by Eq. 13, with
+ * t_dec = number of earlier decode steps (the first step is t_dec = 0).  Writes
+ * out (float32) and, when non-NULL, sel and the dbg arrays; inserts (q_bar,
+ * support) into every head's cache.  len must satisfy 1 <= len <= max_len and
+ * must not decrease between calls (RETOPK_ERR_STATE otherwise). */
+retopk_status retopk_decode_step(retopk_handle h, const void *q, const void *k, const void *v,
+                                 int64_t len, float *out, int32_t *sel,
+                                 const retopk_debug *dbg, void *stream);
+
+/* Exact Top-K attention (Eq. 1 with Eq. 4, then Eq. 12) for every head over rows
+ * [0, len): the full-history baseline.  Uses the handle's workspaces only; the
+ * caches and counters are untouched. */
+retopk_status exact_topk_attention(retopk_handle h, const void *q, const void *k,
+                                   const void *v, int64_t len, float *out, int32_t *sel,
+                                   void *stream);
+
+/* Read the cumulative counters (synchronises). */
+retopk_status retopk_stats(retopk_handle h, retopk_stats_t *out);
+
+/* Copy the cache state to host arrays (synchronises):
+ * qbar [B*Hq, C, d] float, supp [B*Hq, C, K] int32 (-1 padded), cnt [B*Hq, C];
+ * n_inserted = insertions so far, t_dec = decode steps so far.  Any pointer may
+ * be NULL. */
+retopk_status retopk_get_state(retopk_handle h, float *qbar, int32_t *supp, int32_t *cnt,
+                               int64_t *n_inserted, int64_t *t_dec);
+
+/* Replace the cache state from host arrays laid out as in retopk_get_state
+ * (synchronous).  Resets the counters and the len monotonicity check. */
+retopk_status retopk_set_state(retopk_handle h, const float *qbar, const int32_t *supp,
+                               const int32_t *cnt, int64_t n_inserted, int64_t t_dec);
+
+/* Per-kernel timing with HIP events recorded around each launch, on the launch
+ * stream.  retopk_profile(h, 1) clears and starts recording, retopk_profile(h, 0)
+ * stops.  retopk_profile_read (synchronises) fills, for kernel ids
+ * 0 .. n_kernels-1 (see retopk_kernel_name), the number of launches and their
+ * summed duration in milliseconds; it returns RETOPK_ERR_STATE if more launches
+ * were recorded than the event pool holds (65536). */
+retopk_status retopk_profile(retopk_handle h, int32_t enable);
+retopk_status retopk_profile_read(retopk_handle h, int32_t n_kernels, uint64_t *launches,
+                                  double *total_ms);
+const char *retopk_kernel_name(int32_t kernel_id);   /* NULL past the last id */
+
+const char *retopk_status_string(retopk_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

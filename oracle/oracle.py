@@ -65,6 +65,8 @@ def load(path: str | None = None):
     lib.orc_scores.restype = None
     lib.orc_normalize.argtypes = [P, C.c_int32, P]
     lib.orc_normalize.restype = None
+    lib.orc_attend.argtypes = [P, P, P, C.c_int32, C.c_int64, P, P]
+    lib.orc_attend.restype = None
     if path == _build.LIB:
         _LIB = lib
     return lib
@@ -219,6 +221,17 @@ def scores(q, krows, idx, lib_path: str | None = None) -> np.ndarray:
     idx = np.ascontiguousarray(idx, dtype=np.int32)
     out = np.zeros(idx.shape[0], np.float32)
     lib.orc_scores(_ptr(q), _ptr(krows), q.shape[-1], idx.shape[0], _ptr(idx), _ptr(out))
+    return out
+
+
+def attend(q, krows, vrows, idx, lib_path: str | None = None) -> np.ndarray:
+    """Eq. 10 + Eq. 12 over the index set `idx` (rows of krows/vrows [n, d])."""
+    lib = load(lib_path)
+    q, krows, vrows = _f32(q), _f32(krows), _f32(vrows)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    out = np.zeros(q.shape[-1], np.float32)
+    lib.orc_attend(_ptr(q), _ptr(krows), _ptr(vrows), q.shape[-1], idx.shape[0], _ptr(idx),
+                   _ptr(out))
     return out
 
 

@@ -130,6 +130,19 @@ void orc_scores(const float *q, const float *krows, int32_t d, int64_t n,
         out[t] = qk_score(q, krows + (int64_t)idx[t] * d, d);
 }
 
+void orc_attend(const float *q, const float *krows, const float *vrows, int32_t d, int64_t n,
+                const int32_t *idx, float *out)
+{
+    scored_key *list = (scored_key *)malloc((size_t)(n > 0 ? n : 1) * sizeof(scored_key));
+    for (int64_t t = 0; t < n; ++t) {
+        list[t].s = qk_score(q, krows + (int64_t)idx[t] * d, d);
+        list[t].i = idx[t];
+    }
+    qsort(list, (size_t)n, sizeof(scored_key), cmp_index);
+    softmax_v(list, n, vrows, d, out);
+    free(list);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Exact Top-K attention for one query head (Eq. 1, Eq. 4, Eq. 12)           */
 /* ------------------------------------------------------------------------ */

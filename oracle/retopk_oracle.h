@@ -93,6 +93,12 @@ void orc_scores(const float *q, const float *krows, int32_t d, int64_t n,
                 const int32_t *idx, float *out);
 void orc_normalize(const float *q, int32_t d, float *qbar);
 
+/* Eq. 10 then Eq. 12 over a given index set idx[0..n): the output an attention
+ * step produces when its support is exactly that set (used to check an output
+ * computed on an equally valid near-tie support). */
+void orc_attend(const float *q, const float *krows, const float *vrows, int32_t d, int64_t n,
+                const int32_t *idx, float *out);
+
 #ifdef __cplusplus
 }
 #endif

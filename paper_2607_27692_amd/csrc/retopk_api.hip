@@ -1,0 +1,484 @@
+// retopk_api.hip -- host side of the C ABI declared in include/retopk.h:
+// argument validation, device allocation, the per-step path mode, launch
+// geometry and sequencing, counters, cache state access and event profiling.
+#include "retopk.h"
+#include "retopk_internal.h"
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <vector>
+
+using namespace retopk;
+
+namespace {
+
+constexpr int kProfileMaxLaunches = 65536;
+constexpr int kNumKernels = 3;
+const char *const kKernelNames[kNumKernels] = {"retopk_select", "retopk_score", "retopk_filter"};
+enum { KID_SELECT = 0, KID_SCORE = 1, KID_FILTER = 2 };
+
+}  // namespace
+
+struct retopk_handle_s {
+    retopk_config cfg{};
+    int G = 1;
+    int cand_cap = 0;
+    float inv_sqrt_d = 0.0f;
+    int device = 0;
+    Ws w{};
+    std::vector<void *> allocs;
+    int64_t n_ins = 0;
+    int64_t t_dec = 0;
+    int64_t last_len = 0;
+    bool broken = false;
+    hipStream_t last_stream = nullptr;
+    // host-side counters (paths decided on the host)
+    uint64_t steps = 0, head_steps = 0, refresh = 0, cold = 0, host_scans = 0;
+    // profiling
+    bool prof = false;
+    bool prof_overflow = false;
+    std::vector<hipEvent_t> ev;       // 2 per launch
+    std::vector<int> ev_kernel;
+    size_t ev_used = 0;
+};
+
+namespace {
+
+int64_t heads_of(const retopk_config &c) { return (int64_t)c.batch * c.n_q_heads; }
+size_t elem_size(const retopk_config &c) { return c.dtype == RETOPK_BF16 ? 2 : 4; }
+
+retopk_status validate_config(const retopk_config *c)
+{
+    if (!c) return RETOPK_ERR_ARG;
+    if (c->batch < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1) return RETOPK_ERR_ARG;
+    if (c->n_q_heads % c->n_kv_heads != 0) return RETOPK_ERR_ARG;
+    if (c->dtype != RETOPK_F32 && c->dtype != RETOPK_BF16) return RETOPK_ERR_ARG;
+    if (c->head_dim < 1) return RETOPK_ERR_ARG;
+    if (c->max_len < 1 || c->max_len >= ((int64_t)1 << 31)) return RETOPK_ERR_ARG;
+    if (c->k < 1 || c->cache_cap < 0 || c->r < 1 || c->window < 0 || c->refresh < 0)
+        return RETOPK_ERR_ARG;
+    if (!std::isfinite(c->tau)) return RETOPK_ERR_ARG;
+    if (c->k > kMaxK || c->cache_cap > kMaxCache || c->r > kMaxR) return RETOPK_ERR_UNSUPPORTED;
+    if ((int64_t)c->r * c->k + c->window >= ((int64_t)1 << 30)) return RETOPK_ERR_UNSUPPORTED;
+    if (!shape_supported(c->dtype, c->head_dim, c->n_q_heads / c->n_kv_heads))
+        return RETOPK_ERR_UNSUPPORTED;
+    return RETOPK_OK;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+template <typename T>
+retopk_status alloc(retopk_handle h, T **out, size_t count)
+{
+    void *p = nullptr;
+    size_t bytes = count * sizeof(T);
+    if (bytes == 0) bytes = sizeof(T);
+    if (hipMalloc(&p, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return RETOPK_ERR_OOM;
+    }
+    h->allocs.push_back(p);
+    if (hipMemset(p, 0, bytes) != hipSuccess) return RETOPK_ERR_HIP;
+    *out = (T *)p;
+    return RETOPK_OK;
+}
+
+StepArgs base_args(const retopk_handle_s *h)
+{
+    const retopk_config &c = h->cfg;
+    StepArgs a{};
+    a.B = c.batch;
+    a.Hq = c.n_q_heads;
+    a.Hkv = c.n_kv_heads;
+    a.G = h->G;
+    a.D = c.head_dim;
+    a.max_len = c.max_len;
+    a.K = c.k;
+    a.M = c.cache_cap;
+    a.R = c.r;
+    a.W = c.window;
+    a.cand_cap = h->cand_cap;
+    a.tau = c.tau;
+    a.inv_sqrt_d = h->inv_sqrt_d;
+    a.q_head_stride = c.head_dim;
+    return a;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Rows per scan block: about 128 blocks per (b, KV head), 256..4096 rows, a
+// multiple of the 256 rows one block pass covers.
+int scan_chunk_rows(int64_t len)
+{
+    int64_t want = ceil_div(len, 128);
+    int64_t rows = 256;
+    while (rows < want && rows < 4096) rows <<= 1;
+    return (int)rows;
+}
+
+Geometry make_geometry(const retopk_handle_s *h, int64_t len, int mode)
+{
+    const retopk_config &c = h->cfg;
+    Geometry g{};
+    g.select_blocks_per_head = c.cache_cap > 0 ? (int)ceil_div(c.cache_cap, kSlotsPerSelectBlock) : 0;
+    g.scan_chunk_rows = scan_chunk_rows(len);
+    g.scan_blocks = (int)((int64_t)c.batch * c.n_kv_heads * ceil_div(len, g.scan_chunk_rows));
+    g.cand_blocks_per_head = mode == MODE_SELECT ? (int)ceil_div(h->cand_cap, kCandRows) : 0;
+    g.filter_blocks_per_head = (int)ceil_div(len, kFilterRows);
+    return g;
+}
+
+retopk_status record(retopk_handle h, hipStream_t s, int kid, bool begin)
+{
+    if (!h->prof) return RETOPK_OK;
+    if (begin) {
+        if (h->ev_used / 2 >= (size_t)kProfileMaxLaunches) {
+            h->prof_overflow = true;
+            return RETOPK_OK;
+        }
+        while (h->ev.size() < h->ev_used + 2) {
+            hipEvent_t e;
+            if (hipEventCreate(&e) != hipSuccess) return RETOPK_ERR_HIP;
+            h->ev.push_back(e);
+        }
+        if (hipEventRecord(h->ev[h->ev_used], s) != hipSuccess) return RETOPK_ERR_HIP;
+        h->ev_kernel.push_back(kid);
+    } else {
+        if (h->ev_kernel.size() * 2 != h->ev_used + 2) return RETOPK_OK;   // begin was dropped
+        if (hipEventRecord(h->ev[h->ev_used + 1], s) != hipSuccess) return RETOPK_ERR_HIP;
+        h->ev_used += 2;
+    }
+    return RETOPK_OK;
+}
+
+retopk_status fail(retopk_handle h)
+{
+    h->broken = true;
+    return RETOPK_ERR_HIP;
+}
+
+// Launches one step (or one prefill query) in `mode`.
+retopk_status run_step(retopk_handle h, const StepArgs &a, int mode, hipStream_t s)
+{
+    const Geometry geo = make_geometry(h, a.len, mode);
+    const int dt = h->cfg.dtype;
+    retopk_status st;
+    if (mode == MODE_SELECT) {
+        if ((st = record(h, s, KID_SELECT, true)) != RETOPK_OK) return st;
+        if (launch_select(dt, a, h->w, geo, s) != hipSuccess) return fail(h);
+        if ((st = record(h, s, KID_SELECT, false)) != RETOPK_OK) return st;
+    }
+    if ((st = record(h, s, KID_SCORE, true)) != RETOPK_OK) return st;
+    if (launch_score(dt, a, h->w, geo, s) != hipSuccess) return fail(h);
+    if ((st = record(h, s, KID_SCORE, false)) != RETOPK_OK) return st;
+    if ((st = record(h, s, KID_FILTER, true)) != RETOPK_OK) return st;
+    if (launch_filter(dt, a, h->w, geo, s) != hipSuccess) return fail(h);
+    if ((st = record(h, s, KID_FILTER, false)) != RETOPK_OK) return st;
+    return RETOPK_OK;
+}
+
+retopk_status sync_last(retopk_handle h)
+{
+    if (hipSetDevice(h->device) != hipSuccess) return RETOPK_ERR_HIP;
+    if (hipStreamSynchronize(h->last_stream) != hipSuccess) return fail(h);
+    return RETOPK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *retopk_status_string(retopk_status s)
+{
+    switch (s) {
+    case RETOPK_OK: return "ok";
+    case RETOPK_ERR_ARG: return "invalid argument";
+    case RETOPK_ERR_UNSUPPORTED: return "unsupported shape";
+    case RETOPK_ERR_OOM: return "device out of memory";
+    case RETOPK_ERR_HIP: return "HIP runtime error";
+    case RETOPK_ERR_STATE: return "call out of order or handle broken";
+    }
+    return "unknown status";
+}
+
+const char *retopk_kernel_name(int32_t kernel_id)
+{
+    return (kernel_id >= 0 && kernel_id < kNumKernels) ? kKernelNames[kernel_id] : nullptr;
+}
+
+retopk_status retopk_create(const retopk_config *cfg, retopk_handle *out)
+{
+    if (!out) return RETOPK_ERR_ARG;
+    *out = nullptr;
+    retopk_status st = validate_config(cfg);
+    if (st != RETOPK_OK) return st;
+    retopk_handle h = new (std::nothrow) retopk_handle_s();
+    if (!h) return RETOPK_ERR_OOM;
+    h->cfg = *cfg;
+    h->G = cfg->n_q_heads / cfg->n_kv_heads;
+    h->cand_cap = cfg->r * cfg->k + cfg->window;
+    h->inv_sqrt_d = (float)(1.0 / std::sqrt((double)cfg->head_dim));
+    if (hipGetDevice(&h->device) != hipSuccess) {
+        delete h;
+        return RETOPK_ERR_HIP;
+    }
+    const int64_t BH = heads_of(*cfg);
+    const int64_t C = cfg->cache_cap, D = cfg->head_dim, K = cfg->k, L = cfg->max_len;
+    Ws &w = h->w;
+    if ((st = alloc(h, &w.qbar, (size_t)(BH * C * D))) != RETOPK_OK ||
+        (st = alloc(h, &w.supp, (size_t)(BH * C * K))) != RETOPK_OK ||
+        (st = alloc(h, &w.cnt, (size_t)(BH * C))) != RETOPK_OK ||
+        (st = alloc(h, &w.scores, (size_t)(BH * L))) != RETOPK_OK ||
+        (st = alloc(h, &w.surv, (size_t)(BH * L))) != RETOPK_OK ||
+        (st = alloc(h, &w.hist, (size_t)(BH * kHistBins))) != RETOPK_OK ||
+        (st = alloc(h, &w.cand, (size_t)(BH * h->cand_cap))) != RETOPK_OK ||
+        (st = alloc(h, &w.cand_ent, (size_t)(BH * h->cand_cap))) != RETOPK_OK ||
+        (st = alloc(h, &w.rho, (size_t)(BH * C))) != RETOPK_OK ||
+        (st = alloc(h, &w.path, (size_t)BH)) != RETOPK_OK ||
+        (st = alloc(h, &w.n_cand, (size_t)BH)) != RETOPK_OK ||
+        (st = alloc(h, &w.ctr_select, (size_t)BH)) != RETOPK_OK ||
+        (st = alloc(h, &w.ctr_cand, (size_t)BH)) != RETOPK_OK ||
+        (st = alloc(h, &w.ctr_filter, (size_t)BH)) != RETOPK_OK ||
+        (st = alloc(h, &w.surv_count, (size_t)BH)) != RETOPK_OK ||
+        (st = alloc(h, &w.stats, (size_t)STAT_COUNT)) != RETOPK_OK) {
+        retopk_destroy(h);
+        return st;
+    }
+    if (hipDeviceSynchronize() != hipSuccess) {
+        retopk_destroy(h);
+        return RETOPK_ERR_HIP;
+    }
+    *out = h;
+    return RETOPK_OK;
+}
+
+retopk_status retopk_destroy(retopk_handle h)
+{
+    if (!h) return RETOPK_OK;
+    (void)hipSetDevice(h->device);
+    if (!h->allocs.empty()) (void)hipDeviceSynchronize();
+    for (void *p : h->allocs) (void)hipFree(p);
+    for (hipEvent_t e : h->ev) (void)hipEventDestroy(e);
+    delete h;
+    return RETOPK_OK;
+}
+
+retopk_status retopk_decode_step(retopk_handle h, const void *q, const void *k, const void *v,
+                                 int64_t len, float *out, int32_t *sel,
+                                 const retopk_debug *dbg, void *stream)
+{
+    if (!h || !q || !k || !v || !out) return RETOPK_ERR_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return RETOPK_ERR_ARG;
+    if (len < 1 || len > h->cfg.max_len) return RETOPK_ERR_ARG;
+    if (h->broken || len < h->last_len) return RETOPK_ERR_STATE;
+    const retopk_config &c = h->cfg;
+    const int64_t n_valid = h->n_ins < c.cache_cap ? h->n_ins : c.cache_cap;
+    const bool refresh = c.refresh > 0 && h->t_dec > 0 && h->t_dec % c.refresh == 0;
+    const int mode = n_valid == 0 ? MODE_COLD : (refresh ? MODE_REFRESH : MODE_SELECT);
+
+    StepArgs a = base_args(h);
+    a.mode = mode;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.len = len;
+    a.out = out;
+    a.sel = sel;
+    a.n_ins = h->n_ins;
+    a.insert_slot = c.cache_cap > 0 ? (int32_t)(h->n_ins % c.cache_cap) : 0;
+    a.do_insert = c.cache_cap > 0 ? 1 : 0;
+    if (dbg) {
+        a.dbg_path = dbg->path;
+        a.dbg_rho = dbg->rho_max;
+        a.dbg_ret = dbg->retrieved;
+        a.dbg_ncand = dbg->n_cand;
+        a.dbg_cand = dbg->cand;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    if (hipSetDevice(h->device) != hipSuccess) return fail(h);
+    retopk_status st = run_step(h, a, mode, s);
+    if (st != RETOPK_OK) return st;
+    h->last_stream = s;
+    h->last_len = len;
+    const int64_t BH = heads_of(c);
+    h->steps += 1;
+    h->head_steps += (uint64_t)BH;
+    if (mode == MODE_REFRESH) h->refresh += (uint64_t)BH;
+    if (mode == MODE_COLD) h->cold += (uint64_t)BH;
+    if (mode != MODE_SELECT) h->host_scans += (uint64_t)c.batch * c.n_kv_heads;
+    if (c.cache_cap > 0) h->n_ins += 1;
+    h->t_dec += 1;
+    return RETOPK_OK;
+}
+
+retopk_status exact_topk_attention(retopk_handle h, const void *q, const void *k,
+                                   const void *v, int64_t len, float *out, int32_t *sel,
+                                   void *stream)
+{
+    if (!h || !q || !k || !v || !out) return RETOPK_ERR_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return RETOPK_ERR_ARG;
+    if (len < 1 || len > h->cfg.max_len) return RETOPK_ERR_ARG;
+    if (h->broken) return RETOPK_ERR_STATE;
+    StepArgs a = base_args(h);
+    a.mode = MODE_EXACT;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.len = len;
+    a.out = out;
+    a.sel = sel;
+    a.do_insert = 0;
+    hipStream_t s = (hipStream_t)stream;
+    if (hipSetDevice(h->device) != hipSuccess) return fail(h);
+    retopk_status st = run_step(h, a, MODE_EXACT, s);
+    if (st != RETOPK_OK) return st;
+    h->last_stream = s;
+    return RETOPK_OK;
+}
+
+retopk_status retopk_prefill_init(retopk_handle h, const void *q_tail, int32_t n,
+                                  const void *k, const void *v, int64_t prefill_len,
+                                  void *stream)
+{
+    if (!h || !k || !v || (n > 0 && !q_tail)) return RETOPK_ERR_ARG;
+    if (n < 0 || prefill_len < n || prefill_len > h->cfg.max_len) return RETOPK_ERR_ARG;
+    if ((q_tail && !aligned16(q_tail)) || !aligned16(k) || !aligned16(v)) return RETOPK_ERR_ARG;
+    if (h->broken) return RETOPK_ERR_STATE;
+    const retopk_config &c = h->cfg;
+    if (c.cache_cap == 0 || n == 0) return RETOPK_OK;
+    hipStream_t s = (hipStream_t)stream;
+    if (hipSetDevice(h->device) != hipSuccess) return fail(h);
+    const size_t es = elem_size(c);
+    for (int32_t u = 0; u < n; ++u) {
+        StepArgs a = base_args(h);
+        a.mode = MODE_PREFILL;
+        a.q = (const char *)q_tail + (size_t)u * c.head_dim * es;
+        a.q_head_stride = (int64_t)n * c.head_dim;
+        a.k = k;
+        a.v = v;
+        a.len = prefill_len - n + u + 1;
+        a.out = nullptr;
+        a.sel = nullptr;
+        a.n_ins = h->n_ins;
+        a.insert_slot = (int32_t)(h->n_ins % c.cache_cap);
+        a.do_insert = 1;
+        retopk_status st = run_step(h, a, MODE_PREFILL, s);
+        if (st != RETOPK_OK) return st;
+        h->n_ins += 1;
+    }
+    h->last_stream = s;
+    return RETOPK_OK;
+}
+
+retopk_status retopk_stats(retopk_handle h, retopk_stats_t *out)
+{
+    if (!h || !out) return RETOPK_ERR_ARG;
+    retopk_status st = sync_last(h);
+    if (st != RETOPK_OK) return st;
+    unsigned long long dev[STAT_COUNT];
+    if (hipMemcpy(dev, h->w.stats, sizeof(dev), hipMemcpyDeviceToHost) != hipSuccess) return fail(h);
+    out->steps = h->steps;
+    out->head_steps = h->head_steps;
+    out->reuse = dev[STAT_REUSE];
+    out->fallback = dev[STAT_FALLBACK];
+    out->refresh = h->refresh;
+    out->cold = h->cold;
+    out->kv_group_scans = dev[STAT_SCANS] + h->host_scans;
+    out->cand_sum = dev[STAT_CAND_SUM];
+    out->cand_max = dev[STAT_CAND_MAX];
+    return RETOPK_OK;
+}
+
+retopk_status retopk_get_state(retopk_handle h, float *qbar, int32_t *supp, int32_t *cnt,
+                               int64_t *n_inserted, int64_t *t_dec)
+{
+    if (!h) return RETOPK_ERR_ARG;
+    retopk_status st = sync_last(h);
+    if (st != RETOPK_OK) return st;
+    const retopk_config &c = h->cfg;
+    const size_t e = (size_t)heads_of(c) * c.cache_cap;
+    if (qbar && e && hipMemcpy(qbar, h->w.qbar, e * c.head_dim * sizeof(float),
+                               hipMemcpyDeviceToHost) != hipSuccess)
+        return fail(h);
+    if (supp && e && hipMemcpy(supp, h->w.supp, e * c.k * sizeof(int32_t),
+                               hipMemcpyDeviceToHost) != hipSuccess)
+        return fail(h);
+    if (cnt && e && hipMemcpy(cnt, h->w.cnt, e * sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess)
+        return fail(h);
+    if (n_inserted) *n_inserted = h->n_ins;
+    if (t_dec) *t_dec = h->t_dec;
+    return RETOPK_OK;
+}
+
+retopk_status retopk_set_state(retopk_handle h, const float *qbar, const int32_t *supp,
+                               const int32_t *cnt, int64_t n_inserted, int64_t t_dec)
+{
+    if (!h || n_inserted < 0 || t_dec < 0) return RETOPK_ERR_ARG;
+    const retopk_config &c = h->cfg;
+    const size_t e = (size_t)heads_of(c) * c.cache_cap;
+    if (e && (!qbar || !supp || !cnt)) return RETOPK_ERR_ARG;
+    for (size_t i = 0; i < e; ++i) {
+        if (cnt[i] < 0 || cnt[i] > c.k) return RETOPK_ERR_ARG;
+        for (int t = 0; t < cnt[i]; ++t) {
+            int32_t x = supp[i * c.k + t];
+            if (x < 0 || x >= c.max_len) return RETOPK_ERR_ARG;
+        }
+        for (int j = 0; j < c.head_dim; ++j)
+            if (!std::isfinite(qbar[i * c.head_dim + j])) return RETOPK_ERR_ARG;
+    }
+    if (h->broken) return RETOPK_ERR_STATE;
+    retopk_status st = sync_last(h);
+    if (st != RETOPK_OK) return st;
+    if (e) {
+        if (hipMemcpy(h->w.qbar, qbar, e * c.head_dim * sizeof(float), hipMemcpyHostToDevice) != hipSuccess ||
+            hipMemcpy(h->w.supp, supp, e * c.k * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess ||
+            hipMemcpy(h->w.cnt, cnt, e * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess)
+            return fail(h);
+    }
+    if (hipMemset(h->w.stats, 0, STAT_COUNT * sizeof(unsigned long long)) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess)
+        return fail(h);
+    h->n_ins = c.cache_cap > 0 ? n_inserted : 0;
+    h->t_dec = t_dec;
+    h->last_len = 0;
+    h->steps = h->head_steps = h->refresh = h->cold = h->host_scans = 0;
+    return RETOPK_OK;
+}
+
+retopk_status retopk_profile(retopk_handle h, int32_t enable)
+{
+    if (!h) return RETOPK_ERR_ARG;
+    h->prof = enable != 0;
+    if (h->prof) {
+        h->ev_used = 0;
+        h->ev_kernel.clear();
+        h->prof_overflow = false;
+    }
+    return RETOPK_OK;
+}
+
+retopk_status retopk_profile_read(retopk_handle h, int32_t n_kernels, uint64_t *launches,
+                                  double *total_ms)
+{
+    if (!h || n_kernels < 0 || (n_kernels > 0 && (!launches || !total_ms))) return RETOPK_ERR_ARG;
+    for (int i = 0; i < n_kernels; ++i) {
+        launches[i] = 0;
+        total_ms[i] = 0.0;
+    }
+    retopk_status st = sync_last(h);
+    if (st != RETOPK_OK) return st;
+    for (size_t i = 0; i < h->ev_used / 2; ++i) {
+        float ms = 0.0f;
+        if (hipEventElapsedTime(&ms, h->ev[2 * i], h->ev[2 * i + 1]) != hipSuccess) return fail(h);
+        const int kid = h->ev_kernel[i];
+        if (kid < n_kernels) {
+            launches[kid] += 1;
+            total_ms[kid] += ms;
+        }
+    }
+    return h->prof_overflow ? RETOPK_ERR_STATE : RETOPK_OK;
+}
+
+}  // extern "C"

@@ -204,23 +204,29 @@ def make_inputs(w: Workload, seed: int | None = None) -> Inputs:
     )
 
 
-def make_support_state(inp: Inputs, seed: int = 1) -> tuple[np.ndarray, np.ndarray]:
+def make_support_state(inp: Inputs, seed: int = 1,
+                       heads: list[int] | None = None) -> tuple[np.ndarray, np.ndarray]:
     """A seeded, valid cache of supports without running any selection.
 
     For each (sequence, query head) and cache slot u (holding prompt-tail query u),
     draws K distinct key indices below the query's causal length, half of them from
     the key cluster the query walked to and the rest uniformly.  Returns
     (supp [B*Hq, C, K] int32 ascending, cnt [B*Hq, C] int32).  It lets a full-size
-    test start a decode step from a plausible cache state at once.
+    test start a decode step from a plausible cache state at once.  With `heads`
+    (flat b*Hq + h indices) only those heads are drawn; the others hold empty
+    supports.
     """
     w = inp.w
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
     C, K = w.cache_cap, w.k
-    supp = np.empty((w.batch * w.n_q_heads, C, K), np.int32)
-    cnt = np.full((w.batch * w.n_q_heads, C), K, np.int32)
+    supp = np.full((w.batch * w.n_q_heads, C, K), -1, np.int32)
+    cnt = np.zeros((w.batch * w.n_q_heads, C), np.int32)
     for b in range(w.batch):
         for h in range(w.n_q_heads):
+            if heads is not None and b * w.n_q_heads + h not in heads:
+                continue
             g = h // w.group
+            cnt[b * w.n_q_heads + h] = K
             zk = inp.centre_of_key[b, g]
             for u in range(C):
                 lim = w.prompt_len - C + u + 1

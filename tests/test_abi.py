@@ -1,0 +1,74 @@
+"""The C ABI library loads, exports every function include/retopk.h declares, and
+rejects bad arguments on the host before touching a device (no GPU needed)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2607_27692_amd import build as B
+from paper_2607_27692_amd import retopk as R
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "retopk.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB):
+        B.build()
+    return R.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b([a-z_]+)\s*\(", text)) - {"if", "sizeof"})
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(R.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4, -5):
+        assert R.retopk_status_string(code) == R.STATUS[code]
+    assert R.retopk_kernel_name(0) == "retopk_select"
+    assert R.retopk_kernel_name(99) is None
+
+
+def _cfg(**kw):
+    base = dict(batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128, max_len=4096, k=256,
+                cache_cap=256, r=4, window=128, tau=0.8, refresh=32, dtype="bf16")
+    base.update(kw)
+    return R.make_config(**base)
+
+
+@pytest.mark.parametrize("bad, code", [
+    (dict(batch=0), -1), (dict(n_q_heads=30), -1), (dict(n_kv_heads=0), -1),
+    (dict(max_len=0), -1), (dict(max_len=1 << 31), -1), (dict(k=0), -1),
+    (dict(cache_cap=-1), -1), (dict(r=0), -1), (dict(window=-1), -1), (dict(refresh=-1), -1),
+    (dict(tau=float("nan")), -1), (dict(tau=float("inf")), -1), (dict(dtype=7), -1),
+    (dict(head_dim=96), -2), (dict(n_q_heads=24, n_kv_heads=8), -2), (dict(k=4096), -2),
+    (dict(r=64), -2), (dict(cache_cap=8192), -2),
+])
+def test_create_rejects_bad_config(lib, bad, code):
+    h = C.c_void_p()
+    cfg = _cfg(**bad)
+    assert lib.retopk_create(C.byref(cfg), C.byref(h)) == code
+    assert h.value is None
+
+
+def test_null_arguments(lib):
+    assert lib.retopk_create(None, None) == -1
+    assert lib.retopk_destroy(None) == 0
+    assert lib.retopk_decode_step(None, 16, 16, 16, 1, 16, None, None, None) == -1
+    assert lib.exact_topk_attention(None, 16, 16, 16, 1, 16, None, None) == -1
+    assert lib.retopk_prefill_init(None, 16, 1, 16, 16, 1, None) == -1
+    st = R.retopk_stats_t()
+    assert lib.retopk_stats(None, C.byref(st)) == -1
+    assert lib.retopk_profile(None, 1) == -1

@@ -1,0 +1,224 @@
+"""GPU parity of the ReTopK decode step (Sec. 3.3-3.4) against the oracle.
+
+Lock-step protocol: before every step the GPU handle is loaded with the oracle's
+cache state (oracle -> GPU only), both run the same step, and everything the step
+decides is compared: path (Eq. 13), rho_max and retrieved slots (Eq. 6-7), the
+candidate set (Eq. 8-9), the selected support (Eq. 10-11), the output (Eq. 12)
+and the inserted cache entry (Sec. 3.4).  A step can never inherit a difference
+from an earlier one.  Separately the GPU runs its own trajectory from its own
+prefill initialisation, which must agree with the oracle's until the first
+near-tie, and be bitwise reproducible."""
+import numpy as np
+import pytest
+
+from gpu_harness import (REL_GAP, RHO_TIE, Tally, check_output, check_selection, debug_buffers,
+                         handle_of, params_of, to_dev, torch_cuda)
+from oracle import oracle as O
+from paper_2607_27692_amd.inputs import WORKLOADS, make_inputs, make_support_state
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev_inputs(inp):
+    return dict(q_tail=to_dev(inp.q_tail_raw), q_dec=to_dev(inp.q_dec_raw), k=to_dev(inp.k_raw),
+                v=to_dev(inp.v_raw))
+
+
+def _compare_step(t, w, p, inp, gpu, orc_res, pre_state, heads, tally, q_host):
+    """gpu: dict of numpy arrays read back after the GPU step; orc_res: (out, sel, info)."""
+    o_out, o_sel, info = orc_res
+    L = w.step_len(t)
+    G = w.group
+    for bh in heads:
+        b, h = divmod(bh, w.n_q_heads)
+        where = f"step {t} b={b} h={h}"
+        q = q_host[b, h]
+        kr, vr = inp.k[b, h // G], inp.v[b, h // G]
+        opath, gpath = int(info.path[bh]), int(gpu["path"][bh])
+        if opath != gpath:
+            assert {opath, gpath} == {O.REUSE, O.FALLBACK}, f"{where}: path {gpath} vs {opath}"
+            assert abs(info.rho_max[bh] - w.tau) <= REL_GAP, f"{where}: path differs away from tau"
+            tally.path_tie += 1
+            continue
+        if opath in (O.REUSE, O.FALLBACK):
+            assert abs(gpu["rho_max"][bh] - info.rho_max[bh]) <= 1e-12, (
+                f"{where}: rho_max {gpu['rho_max'][bh]!r} vs {info.rho_max[bh]!r}")
+        else:
+            assert np.isnan(gpu["rho_max"][bh])
+        if opath == O.REUSE:
+            gret, oret = gpu["retrieved"][bh], info.retrieved[bh]
+            if not np.array_equal(gret, oret):
+                nv = min(pre_state["n_inserted"], w.cache_cap)
+                qb = O.normalize(q).astype(np.float64)
+                rho = pre_state["qbar"][bh, :nv].astype(np.float64) @ qb
+                rr = rho[oret[oret >= 0]]
+                others = np.delete(rho, oret[oret >= 0])
+                assert others.size and rr.min() - others.max() <= RHO_TIE, (
+                    f"{where}: retrieved {gret} vs {oret}")
+                tally.rho_tie += 1
+                continue
+            n = int(info.n_cand[bh])
+            assert int(gpu["n_cand"][bh]) == n, f"{where}: n_cand {gpu['n_cand'][bh]} vs {n}"
+            assert np.array_equal(gpu["cand"][bh, :n], info.cand[bh, :n]), f"{where}: candidates"
+            assert (gpu["cand"][bh, n:] == -1).all()
+            universe = info.cand[bh, :n]
+        else:
+            assert int(gpu["n_cand"][bh]) == 0 and (gpu["retrieved"][bh] == -1).all()
+            universe = np.arange(L, dtype=np.int32)
+        us = O.scores(q, kr, universe)
+        gsup = check_selection(gpu["sel"][b, h], o_sel[b, h], universe, us, where, tally)
+        exact_set = np.array_equal(gsup, o_sel[b, h][o_sel[b, h] >= 0])
+        check_output(gpu["out"][b, h], q, kr, vr, gsup, o_out[b, h], exact_set, w.dtype, where,
+                     tally)
+        # inserted cache entry
+        slot = pre_state["n_inserted"] % w.cache_cap
+        gq = gpu["state"]["qbar"][bh, slot]
+        oq = O.normalize(q)
+        assert np.array_equal(gq.view(np.uint32), oq.view(np.uint32)) or \
+            np.abs(gq.view(np.int32) - oq.view(np.int32)).max() <= 1, f"{where}: inserted q_bar"
+        gs = gpu["state"]["supp"][bh, slot]
+        assert np.array_equal(gs[gs >= 0], gsup) and (gs[len(gsup):] == -1).all()
+        assert int(gpu["state"]["cnt"][bh, slot]) == len(gsup)
+
+
+def _lockstep(w, inp, p, heads, n_steps, state0=None):
+    torch = torch_cuda()
+    mask = np.zeros(p.heads, np.uint8)
+    mask[heads] = 1
+    orc = O.Oracle(p)
+    if state0 is None:
+        orc.prefill_init(inp.q_tail, inp.k, inp.v, w.prompt_len, head_mask=mask)
+    else:
+        orc.set_state(*state0)
+    dev = _dev_inputs(inp)
+    h = handle_of(p, w.dtype)
+    out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    sel = torch.empty((w.batch, w.n_q_heads, w.k), dtype=torch.int32, device="cuda")
+    dbg = debug_buffers(p)
+    tally = Tally()
+    paths = []
+    for t in range(n_steps):
+        pre = orc.get_state()
+        h.set_state(pre["qbar"], pre["supp"], pre["cnt"], pre["n_inserted"], pre["t_dec"])
+        L = w.step_len(t)
+        h.decode_step(dev["q_dec"][t], dev["k"], dev["v"], L, out, sel, dbg)
+        res = orc.decode_step(inp.q_dec[t], inp.k, inp.v, L, head_mask=mask)
+        torch.cuda.synchronize()
+        gpu = {k_: v_.cpu().numpy() for k_, v_ in dbg.items()}
+        gpu["out"], gpu["sel"] = out.cpu().numpy(), sel.cpu().numpy()
+        gpu["state"] = h.get_state()
+        _compare_step(t, w, p, inp, gpu, res, pre, heads, tally, inp.q_dec[t])
+        paths.append(res[2].path[heads].copy())
+    h.close()
+    return tally, np.array(paths)
+
+
+def test_decode_lockstep_small():
+    """The fp32 single-head workload, all 64 steps, from the oracle's prefill state."""
+    w = WORKLOADS["tiny"]
+    print(f"decode lock-step {w.name}", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w)
+    tally, paths = _lockstep(w, inp, p, [0], w.steps)
+    print(tally, flush=True)
+    assert (paths == O.REUSE).sum() > 20 and (paths == O.FALLBACK).sum() > 0
+    assert (paths == O.REFRESH).sum() == (w.steps - 1) // w.refresh
+    assert tally.exact >= w.steps - 2
+
+
+def test_decode_lockstep_16k_two_groups():
+    """32 query heads on 8 KV heads at 16K, bf16: KV groups 0 and 7 (8 query heads)
+    checked on all 128 steps."""
+    w = WORKLOADS["16k"]
+    print(f"decode lock-step {w.name}", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w)
+    heads = list(range(0, 4)) + list(range(28, 32))
+    tally, paths = _lockstep(w, inp, p, heads, w.steps)
+    print(tally, flush=True)
+    assert (paths == O.REUSE).sum() > 100 and (paths == O.FALLBACK).sum() > 0
+    assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * w.steps
+
+
+@pytest.mark.parametrize("name", ["32k", "128k"])
+def test_decode_full_size_sampled(name):
+    """Full-size layer shapes: the cache starts from the prompt-tail queries with
+    seeded supports (no prefill), and 3 steps run in lock-step; KV groups 0 and
+    Hkv-1 are compared."""
+    w = WORKLOADS[name]
+    print(f"decode full-size {w.name}", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w)
+    supp, cnt = make_support_state(inp)
+    qbar = np.stack([np.stack([O.normalize(inp.q_tail[b, h, u]) for u in range(w.cache_cap)])
+                     for b in range(w.batch) for h in range(w.n_q_heads)])
+    heads = list(range(0, w.group)) + list(range(w.n_q_heads - w.group, w.n_q_heads))
+    tally, paths = _lockstep(w, inp, p, heads, 3,
+                             state0=(qbar, supp, cnt, w.cache_cap, 1))
+    print(tally, paths.tolist(), flush=True)
+    assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * 3
+
+
+def _free_run(w, inp, dev, n_steps):
+    torch = torch_cuda()
+    p = params_of(w)
+    h = handle_of(p, w.dtype)
+    h.prefill_init(dev["q_tail"], w.cache_cap, dev["k"], dev["v"], w.prompt_len)
+    out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    sel = torch.empty((w.batch, w.n_q_heads, w.k), dtype=torch.int32, device="cuda")
+    dbg = debug_buffers(p)
+    outs, sels, paths = [], [], []
+    state0 = h.get_state()
+    for t in range(n_steps):
+        h.decode_step(dev["q_dec"][t], dev["k"], dev["v"], w.step_len(t), out, sel, dbg)
+        outs.append(out.cpu().numpy())
+        sels.append(sel.cpu().numpy())
+        paths.append(dbg["path"].cpu().numpy())
+    st = h.stats()
+    h.close()
+    return state0, np.array(outs), np.array(sels), np.array(paths), st
+
+
+def test_prefill_and_free_running_trajectory_small():
+    """GPU prefill initialisation equals the oracle's (Sec. 3.3), and the GPU's own
+    64-step trajectory follows the oracle's while no near-tie intervenes."""
+    w = WORKLOADS["tiny"]
+    print(f"free-running {w.name}", flush=True)
+    inp = make_inputs(w)
+    dev = _dev_inputs(inp)
+    p = params_of(w)
+    orc = O.Oracle(p)
+    orc.prefill_init(inp.q_tail, inp.k, inp.v, w.prompt_len)
+    ost = orc.get_state()
+    gst, outs, sels, paths, stats = _free_run(w, inp, dev, w.steps)
+    assert gst["n_inserted"] == ost["n_inserted"] == w.cache_cap
+    assert np.array_equal(gst["supp"], ost["supp"])
+    assert np.array_equal(gst["cnt"], ost["cnt"])
+    assert np.abs(gst["qbar"].view(np.int32) - ost["qbar"].view(np.int32)).max() <= 1
+    agree = 0
+    for t in range(w.steps):
+        o_out, o_sel, info = orc.decode_step(inp.q_dec[t], inp.k, inp.v, w.step_len(t))
+        if not (np.array_equal(sels[t], o_sel) and np.array_equal(paths[t], info.path)):
+            break
+        assert np.abs(outs[t] - o_out).max() <= 1e-5 * np.abs(o_out).max()
+        agree += 1
+    print(f"trajectory agrees for {agree} of {w.steps} steps; stats {stats}", flush=True)
+    assert agree >= w.steps // 2
+    assert stats["steps"] == w.steps and stats["head_steps"] == w.steps
+    assert stats["reuse"] + stats["fallback"] + stats["refresh"] + stats["cold"] == w.steps
+    assert stats["refresh"] == (w.steps - 1) // w.refresh
+
+
+def test_determinism_16k():
+    """Two GPU runs of the same 16K trajectory (prefill + 32 steps) are bitwise equal."""
+    w = WORKLOADS["16k"]
+    print(f"determinism {w.name}", flush=True)
+    inp = make_inputs(w)
+    dev = _dev_inputs(inp)
+    a = _free_run(w, inp, dev, 32)
+    b = _free_run(w, inp, dev, 32)
+    for x, y in zip(a[1:4], b[1:4]):
+        assert np.array_equal(x, y)
+    for key in ("qbar", "supp", "cnt"):
+        assert np.array_equal(a[0][key], b[0][key])
+    assert a[4] == b[4]

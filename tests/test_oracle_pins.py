@@ -491,3 +491,15 @@ def test_window_only_reuse_when_supports_empty(oracle_lib):
     s = O.scores(q[0, 0], k[0, 0], np.arange(L - 6, L))
     best = np.sort(np.arange(L - 6, L)[np.lexsort((np.arange(6), -s.astype(np.float64)))[:3]])
     assert sel[0, 0].tolist() == best.tolist()
+
+
+def test_attend_on_given_set_matches_exact(oracle_lib, golden):
+    """orc_attend over the exact support reproduces the exact output, and over the
+    hand case's index sets gives the closed forms of Eq. 12."""
+    k = np.array(golden["keys"], np.float32)
+    v = np.array(golden["values"], np.float32)
+    q = np.array(golden["exact"]["q"], np.float32)
+    for case in golden["exact"]["cases"]:
+        idx = np.array([i for i in case["sel"] if i >= 0], np.int32)
+        want = np.array([_closed(s) for s in case["out"]])
+        np.testing.assert_allclose(O.attend(q, k, v, idx[::-1].copy()), want, rtol=2e-7, atol=1e-7)
