@@ -15,9 +15,10 @@ using namespace retopk;
 namespace {
 
 constexpr int kProfileMaxLaunches = 65536;
-constexpr int kNumKernels = 3;
-const char *const kKernelNames[kNumKernels] = {"retopk_select", "retopk_score", "retopk_filter"};
-enum { KID_SELECT = 0, KID_SCORE = 1, KID_FILTER = 2 };
+constexpr int kNumKernels = 4;
+const char *const kKernelNames[kNumKernels] = {"retopk_select", "retopk_score", "retopk_filter",
+                                               "retopk_final"};
+enum { KID_SELECT = 0, KID_SCORE = 1, KID_FILTER = 2, KID_FINAL = 3 };
 
 }  // namespace
 
@@ -122,7 +123,6 @@ Geometry make_geometry(const retopk_handle_s *h, int64_t len, int mode)
 {
     const retopk_config &c = h->cfg;
     Geometry g{};
-    g.select_blocks_per_head = c.cache_cap > 0 ? (int)ceil_div(c.cache_cap, kSlotsPerSelectBlock) : 0;
     g.scan_chunk_rows = scan_chunk_rows(len);
     g.scan_blocks = (int)((int64_t)c.batch * c.n_kv_heads * ceil_div(len, g.scan_chunk_rows));
     g.cand_blocks_per_head = mode == MODE_SELECT ? (int)ceil_div(h->cand_cap, kCandRows) : 0;
@@ -176,6 +176,9 @@ retopk_status run_step(retopk_handle h, const StepArgs &a, int mode, hipStream_t
     if ((st = record(h, s, KID_FILTER, true)) != RETOPK_OK) return st;
     if (launch_filter(dt, a, h->w, geo, s) != hipSuccess) return fail(h);
     if ((st = record(h, s, KID_FILTER, false)) != RETOPK_OK) return st;
+    if ((st = record(h, s, KID_FINAL, true)) != RETOPK_OK) return st;
+    if (launch_final(dt, a, h->w, geo, s) != hipSuccess) return fail(h);
+    if ((st = record(h, s, KID_FINAL, false)) != RETOPK_OK) return st;
     return RETOPK_OK;
 }
 
@@ -235,12 +238,8 @@ retopk_status retopk_create(const retopk_config *cfg, retopk_handle *out)
         (st = alloc(h, &w.hist, (size_t)(BH * kHistBins))) != RETOPK_OK ||
         (st = alloc(h, &w.cand, (size_t)(BH * h->cand_cap))) != RETOPK_OK ||
         (st = alloc(h, &w.cand_ent, (size_t)(BH * h->cand_cap))) != RETOPK_OK ||
-        (st = alloc(h, &w.rho, (size_t)(BH * C))) != RETOPK_OK ||
         (st = alloc(h, &w.path, (size_t)BH)) != RETOPK_OK ||
         (st = alloc(h, &w.n_cand, (size_t)BH)) != RETOPK_OK ||
-        (st = alloc(h, &w.ctr_select, (size_t)BH)) != RETOPK_OK ||
-        (st = alloc(h, &w.ctr_cand, (size_t)BH)) != RETOPK_OK ||
-        (st = alloc(h, &w.ctr_filter, (size_t)BH)) != RETOPK_OK ||
         (st = alloc(h, &w.surv_count, (size_t)BH)) != RETOPK_OK ||
         (st = alloc(h, &w.stats, (size_t)STAT_COUNT)) != RETOPK_OK) {
         retopk_destroy(h);

@@ -13,12 +13,13 @@ constexpr int kHistBins = 2048;
 constexpr int kHistShift = 21;
 
 constexpr int kScoreThreads = 512;    // k_score and k_filter blocks
-constexpr int kSelectThreads = 256;   // k_select blocks
+constexpr int kSelectThreads = 1024;  // k_select: one block per query head
+constexpr int kFinalThreads = 1024;   // k_final: one block per query head
 constexpr int kScanRowsPerIter = 128; // 8 waves x 16 rows
 constexpr int kCandRows = 512;        // candidates scored per k_score candidate block
 constexpr int kFilterRows = 4096;     // scores filtered per k_filter block
-constexpr int kSlotsPerSelectBlock = 64;
 constexpr int kBitmapWords = 8192;    // union bitmap segment: 262144 indices
+constexpr int kEntCache = 6144;       // final-stage entries staged in LDS
 constexpr int kMaxK = 2048;
 constexpr int kMaxR = 32;
 constexpr int kMaxCache = 4096;
@@ -54,13 +55,9 @@ struct Ws {
     uint32_t *hist;       // [BH, kHistBins] score histogram (zero between steps)
     int32_t *cand;        // [BH, cand_cap] candidate set, ascending
     uint64_t *cand_ent;   // [BH, cand_cap] candidate rank keys
-    double *rho;          // [BH, C] cosine similarities
     int8_t *path;         // [BH]
     int32_t *n_cand;      // [BH]
-    uint32_t *ctr_select; // [BH] block-arrival counters (zero between steps)
-    uint32_t *ctr_cand;   // [BH]
-    uint32_t *ctr_filter; // [BH]
-    uint32_t *surv_count; // [BH]
+    uint32_t *surv_count; // [BH] survivors appended by k_filter (zero between steps)
     unsigned long long *stats;  // [STAT_COUNT]
 };
 
@@ -93,7 +90,6 @@ struct StepArgs {
 
 // Launch geometry chosen on the host.
 struct Geometry {
-    int select_blocks_per_head;
     int scan_chunk_rows;
     int scan_blocks;           // B * Hkv * chunks (0 when the mode never scans)
     int cand_blocks_per_head;  // 0 outside MODE_SELECT
@@ -107,6 +103,8 @@ hipError_t launch_score(int dtype, const StepArgs &a, const Ws &w, const Geometr
                         hipStream_t s);
 hipError_t launch_filter(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
                          hipStream_t s);
+hipError_t launch_final(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
+                        hipStream_t s);
 bool shape_supported(int dtype, int d, int g);
 
 }  // namespace retopk

@@ -1,20 +1,22 @@
 // retopk_kernels.hip -- gfx950 (CDNA4) kernels of the ReTopK decode step.
 //
-// One decode step is three launches on the caller's stream:
-//   k_select  per query head: q_bar, cosine similarity to the cached queries
-//             (Eq. 6), rho_max, Top-R (Eq. 7), the path rule (Eq. 13) and, on
-//             reuse, the candidate set of Eq. 8-9 (union through an LDS bitmap,
+// One decode step is four launches on the caller's stream:
+//   k_select  one block per query head: q_bar, cosine similarity to the cached
+//             queries (Eq. 6), rho_max, Top-R (Eq. 7), the path rule (Eq. 13) and,
+//             on reuse, the candidate set of Eq. 8-9 (union through an LDS bitmap,
 //             emitted in ascending order).
 //   k_score   full-history QK scan of every KV group that has an exact head
-//             (Eq. 4; one key row load serves the G query heads of the group),
-//             plus gathered QK on the candidate sets of reuse heads (Eq. 10).  The
-//             last candidate block of a reuse head reranks (Eq. 11), aggregates
-//             Softmax-V (Eq. 12) and inserts into the cache.
-//   k_filter  for every exact head: from the score histogram built by the scan,
-//             keep the scores at or above the bin that holds the K-th largest;
-//             the last block selects the exact Top-K among them (Eq. 1),
-//             aggregates Softmax-V and inserts (Sec. 3.4).
-// Exact Top-K attention alone is k_score (scan only) + k_filter.
+//             (Eq. 4; one key row load serves the G query heads of the group) with
+//             a per-head score histogram, plus gathered QK on the candidate sets
+//             of reuse heads (Eq. 10).
+//   k_filter  for every exact head: keep the scores at or above the histogram bin
+//             that holds the K-th largest.
+//   k_final   one block per query head: Top-K over the head's candidates (Eq. 11)
+//             or surviving scores (Eq. 1), Softmax-V (Eq. 12), outputs, and the
+//             cache insert of Sec. 3.4.
+// Exact Top-K attention alone is k_score (scan only) + k_filter + k_final.
+// Blocks never wait on each other inside a launch: every hand-over between
+// blocks goes through a kernel boundary.
 //
 // Ranking is on the fp32 scaled score fl32(q.k) * fl32(1/sqrt d) with ties to the
 // lower index: every candidate carries a 64-bit rank (score key << 32 | ~index)
@@ -229,6 +231,7 @@ __device__ void block_qbar(const T *q, float *s_qbar, double *red)
 
 template <int D, int NT>
 struct FinalSmem {
+    uint64_t ent[kEntCache];  // the head's entries, when they fit
     uint64_t sel[kMaxK];      // selected (index << 32 | score key), sorted by index
     float wgt[kMaxK];
     float part[NT / 64][D];
@@ -239,10 +242,10 @@ struct FinalSmem {
     uint32_t found_digit, found_above, found_cnt, count;
 };
 
-// Selects the top min(K, n) of ents[0..n) (distinct 64-bit ranks, larger is
+// Selects the top min(K, n) of src[0..n) (distinct 64-bit ranks, larger is
 // better), then sorts them by index.  Returns the number selected.
 template <int D, int NT>
-__device__ int select_topk(const uint64_t *ents, int n, int K, FinalSmem<D, NT> &sm)
+__device__ int select_topk(const uint64_t *src, int n, int K, FinalSmem<D, NT> &sm)
 {
     const int tid = threadIdx.x;
     uint64_t prefix = 0, mask = 0;
@@ -256,7 +259,7 @@ __device__ int select_topk(const uint64_t *ents, int n, int K, FinalSmem<D, NT> 
             for (int i = tid; i < 256; i += NT) sm.hist[i] = 0;
             __syncthreads();
             for (int i = tid; i < n; i += NT) {
-                uint64_t e = ents[i];
+                uint64_t e = src[i];
                 if ((e & mask) == prefix) atomicAdd(&sm.hist[(e >> shift) & 255u], 1u);
             }
             __syncthreads();
@@ -291,7 +294,7 @@ __device__ int select_topk(const uint64_t *ents, int n, int K, FinalSmem<D, NT> 
     if (tid == 0) sm.count = 0;
     __syncthreads();
     for (int i = tid; i < n; i += NT) {
-        uint64_t e = ents[i];
+        uint64_t e = src[i];
         if (all || (e & mask) >= prefix) {
             uint32_t pos = atomicAdd(&sm.count, 1u);
             if (pos < (uint32_t)kMaxK) sm.sel[pos] = ((uint64_t)rank_index(e) << 32) | rank_key(e);
@@ -299,6 +302,7 @@ __device__ int select_topk(const uint64_t *ents, int n, int K, FinalSmem<D, NT> 
     }
     int kp = 1;
     while (kp < kn) kp <<= 1;
+    __syncthreads();
     for (int i = kn + tid; i < kp; i += NT) sm.sel[i] = ~0ull;
     __syncthreads();
     // Bitonic sort (ascending) of sel[0..kp) -> ascending index order.
@@ -321,7 +325,8 @@ __device__ int select_topk(const uint64_t *ents, int n, int K, FinalSmem<D, NT> 
     return kn;
 }
 
-// Softmax-V over the selected rows (Eq. 12), then sel output and cache insert.
+// Top-K of ents[0..n), Softmax-V over the selected rows (Eq. 12), sel output and
+// cache insert.
 template <typename T, int D, int NT>
 __device__ void finalize_head(const StepArgs &a, const Ws &w, int bh, const uint64_t *ents,
                               int n, FinalSmem<D, NT> &sm)
@@ -334,7 +339,13 @@ __device__ void finalize_head(const StepArgs &a, const Ws &w, int bh, const uint
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
 
-    const int kn = select_topk<D, NT>(ents, n, a.K, sm);
+    const uint64_t *src = ents;
+    if (n <= kEntCache) {
+        for (int i = tid; i < n; i += NT) sm.ent[i] = ents[i];
+        __syncthreads();
+        src = sm.ent;
+    }
+    const int kn = select_topk<D, NT>(src, n, a.K, sm);
 
     if (a.out != nullptr && a.mode != MODE_PREFILL) {
         float mx = -INFINITY;
@@ -353,7 +364,7 @@ __device__ void finalize_head(const StepArgs &a, const Ws &w, int bh, const uint
         float acc[EPV];
 #pragma unroll
         for (int e = 0; e < EPV; ++e) acc[e] = 0.0f;
-#pragma unroll 4
+#pragma unroll 8
         for (int t = wave * RPW + sub; t < kn; t += NW * RPW) {
             uint32_t idx = (uint32_t)(sm.sel[t] >> 32);
             uint4 raw = ((const uint4 *)(vbase + (int64_t)idx * D))[vl];
@@ -389,32 +400,14 @@ __device__ void finalize_head(const StepArgs &a, const Ws &w, int bh, const uint
     }
 }
 
-// Release the block's global writes and count its arrival on ctr; returns true in
-// exactly one block, the last of `expected` to arrive, after an acquire fence.
-__device__ __forceinline__ bool arrive_last(uint32_t *ctr, uint32_t expected, uint32_t *s_flag)
-{
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t prev = atomicAdd(ctr, 1u);
-        *s_flag = (prev + 1u == expected) ? 1u : 0u;
-    }
-    __syncthreads();
-    const bool last = *s_flag != 0u;
-    if (last) {
-        __threadfence();
-        if (threadIdx.x == 0) *ctr = 0u;    // ready for the next step
-    }
-    return last;
-}
-
 // ---------------------------------------------------------------------------
-// k_select
+// k_select: one block per query head
 // ---------------------------------------------------------------------------
 
 template <int D>
 struct SelectSmem {
     uint32_t bitmap[kBitmapWords];
+    double rho[kMaxCache];
     float qbar[D];
     double red64[kSelectThreads / 64];
     uint32_t red32[kSelectThreads / 64];
@@ -423,7 +416,6 @@ struct SelectSmem {
     int32_t best_slot[kSelectThreads / 64];
     int32_t ret[kMaxR];
     uint8_t taken[kMaxCache];
-    uint32_t flag;
 };
 
 __device__ __forceinline__ bool better(double ra, int aa, double rb, int ab)
@@ -435,42 +427,44 @@ template <typename T, int D>
 __global__ __launch_bounds__(kSelectThreads) void k_select(StepArgs a, Ws w, Geometry geo)
 {
     constexpr int NT = kSelectThreads;
+    constexpr int NW = NT / 64;
     __shared__ SelectSmem<D> sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bh = blockIdx.x / geo.select_blocks_per_head;
-    const int sb = blockIdx.x % geo.select_blocks_per_head;
+    const int bh = blockIdx.x;
     const int M = a.M;
     const int n_valid = (int)(a.n_ins < (int64_t)M ? a.n_ins : (int64_t)M);
     const T *q = (const T *)a.q + (int64_t)bh * a.q_head_stride;
 
     block_qbar<T, D, NT>(q, sm.qbar, sm.red64);
 
-    // Eq. 6 for this block's 64 slots: 16 slots per wave, 4 lanes per slot row.
+    // Eq. 6: 16 slots per wave pass, 4 lanes per cached row.
     {
         const int p = lane & 3;
-        const int slot = sb * kSlotsPerSelectBlock + wave * 16 + (lane >> 2);
-        double acc = 0.0;
-        if (slot < n_valid) {
-            const float4 *crow = (const float4 *)(w.qbar + ((int64_t)bh * M + slot) * D);
+        const float4 *cache = (const float4 *)(w.qbar + (int64_t)bh * M * D);
+        for (int base = 0; base < n_valid; base += NW * 16) {
+            const int slot = base + wave * 16 + (lane >> 2);
+            float4 c[D / 16];
+#pragma unroll
+            for (int s = 0; s < D / 16; ++s)
+                c[s] = slot < n_valid ? cache[(int64_t)slot * (D / 4) + s * 4 + p]
+                                      : make_float4(0.f, 0.f, 0.f, 0.f);
+            double acc = 0.0;
 #pragma unroll
             for (int s = 0; s < D / 16; ++s) {
-                float4 c = crow[s * 4 + p];
                 const float *qq = &sm.qbar[(s * 4 + p) * 4];
-                acc += (double)c.x * (double)qq[0];
-                acc += (double)c.y * (double)qq[1];
-                acc += (double)c.z * (double)qq[2];
-                acc += (double)c.w * (double)qq[3];
+                acc += (double)c[s].x * (double)qq[0];
+                acc += (double)c[s].y * (double)qq[1];
+                acc += (double)c[s].z * (double)qq[2];
+                acc += (double)c[s].w * (double)qq[3];
             }
+            acc = quad_sum(acc);
+            if (slot < n_valid && p == 0) sm.rho[slot] = acc;
         }
-        acc = quad_sum(acc);
-        if (slot < n_valid && p == 0) w.rho[(int64_t)bh * M + slot] = acc;
     }
+    __syncthreads();
 
-    if (!arrive_last(&w.ctr_select[bh], (uint32_t)geo.select_blocks_per_head, &sm.flag)) return;
-
-    const double *rho = w.rho + (int64_t)bh * M;
     double mx = -INFINITY;
-    for (int i = tid; i < n_valid; i += NT) mx = fmax(mx, rho[i]);
+    for (int i = tid; i < n_valid; i += NT) mx = fmax(mx, sm.rho[i]);
     mx = block_reduce<NT>(mx, sm.red64, [](double x, double y) { return fmax(x, y); });
 
     // Eq. 13 (no refresh in this mode): exact path iff rho_max < tau.
@@ -493,7 +487,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(StepArgs a, Ws w, Geo
         for (int i = tid; i < n_valid; i += NT) {
             if (sm.taken[i]) continue;
             int age = (int)(((a.n_ins - 1 - i) % M + M) % M);
-            if (bs < 0 || better(rho[i], age, br, ba)) { br = rho[i]; ba = age; bs = i; }
+            if (bs < 0 || better(sm.rho[i], age, br, ba)) { br = sm.rho[i]; ba = age; bs = i; }
         }
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) {
@@ -506,7 +500,7 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(StepArgs a, Ws w, Geo
         if (tid == 0) {
             double fr = sm.best_rho[0];
             int fa = sm.best_age[0], fs = sm.best_slot[0];
-            for (int ww = 1; ww < NT / 64; ++ww) {
+            for (int ww = 1; ww < NW; ++ww) {
                 int os = sm.best_slot[ww];
                 if (os >= 0 && (fs < 0 || better(sm.best_rho[ww], sm.best_age[ww], fr, fa))) {
                     fr = sm.best_rho[ww]; fa = sm.best_age[ww]; fs = os;
@@ -583,15 +577,8 @@ __global__ __launch_bounds__(kSelectThreads) void k_select(StepArgs a, Ws w, Geo
 // k_score: full-history scan blocks, then candidate blocks
 // ---------------------------------------------------------------------------
 
-template <int D, int G>
-struct ScoreSmemSize {
-    static constexpr int kHist = G * kHistBins * 4;
-    static constexpr int kFinal = (int)sizeof(FinalSmem<D, kScoreThreads>) + 16;
-    static constexpr int kBytes = kHist > kFinal ? kHist : kFinal;
-};
-
 template <typename T, int D, int G>
-__device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, unsigned char *smem)
+__device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, uint32_t *s_hist)
 {
     using R = RowT<T, D>;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
@@ -611,7 +598,6 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
     if (row0 >= a.len) return;
     if (a.mode == MODE_SELECT && chunk == 0 && tid == 0) atomicAdd(&w.stats[STAT_SCANS], 1ull);
 
-    uint32_t *s_hist = (uint32_t *)smem;
     for (int i = tid; i < G * kHistBins; i += kScoreThreads) s_hist[i] = 0u;
     __syncthreads();
 
@@ -673,9 +659,8 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
     }
 }
 
-template <typename T, int D, int G>
-__device__ void cand_block(const StepArgs &a, const Ws &w, const Geometry &geo, int cb,
-                           unsigned char *smem)
+template <typename T, int D>
+__device__ void cand_block(const StepArgs &a, const Ws &w, const Geometry &geo, int cb)
 {
     using R = RowT<T, D>;
     constexpr int kIters = kCandRows / kScanRowsPerIter;
@@ -683,8 +668,7 @@ __device__ void cand_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
     const int bh = cb / geo.cand_blocks_per_head, cc = cb % geo.cand_blocks_per_head;
     if (w.path[bh] != PATH_REUSE) return;
     const int n = w.n_cand[bh];
-    const int nblk = n > 0 ? (n + kCandRows - 1) / kCandRows : 1;
-    if (cc >= nblk) return;
+    if (cc * kCandRows >= n) return;
     const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
 
     uint4 qv[R::kNV];
@@ -718,50 +702,31 @@ __device__ void cand_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
         s0 = quad_sum(s0);
         if (p == 0 && ci[u] < n) ce[ci[u]] = rank_of(s0 * a.inv_sqrt_d, (uint32_t)cidx[u]);
     }
-
-    auto &sm = *reinterpret_cast<FinalSmem<D, kScoreThreads> *>(smem);
-    uint32_t *s_flag = reinterpret_cast<uint32_t *>(smem + sizeof(FinalSmem<D, kScoreThreads>));
-    if (!arrive_last(&w.ctr_cand[bh], (uint32_t)nblk, s_flag)) return;
-    finalize_head<T, D, kScoreThreads>(a, w, bh, ce, n, sm);
 }
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kScoreThreads) void k_score(StepArgs a, Ws w, Geometry geo)
 {
-    __shared__ __attribute__((aligned(16))) unsigned char smem[ScoreSmemSize<D, G>::kBytes];
+    __shared__ uint32_t s_hist[G * kHistBins];
     if ((int)blockIdx.x < geo.scan_blocks)
-        scan_block<T, D, G>(a, w, geo, smem);
+        scan_block<T, D, G>(a, w, geo, s_hist);
     else
-        cand_block<T, D, G>(a, w, geo, (int)blockIdx.x - geo.scan_blocks, smem);
+        cand_block<T, D>(a, w, geo, (int)blockIdx.x - geo.scan_blocks);
 }
 
 // ---------------------------------------------------------------------------
-// k_filter
+// k_filter: the surviving scores of every exact head
 // ---------------------------------------------------------------------------
 
-template <typename T, int D>
 __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geometry geo)
 {
     constexpr int NT = kScoreThreads;
     static_assert(NT * 4 == kHistBins, "4 histogram bins per thread");
-    __shared__ FinalSmem<D, NT> sm;
-    __shared__ uint32_t s_bstar, s_flag, s_n;
+    __shared__ uint32_t s_red[NT / 64];
+    __shared__ uint32_t s_bstar;
     const int tid = threadIdx.x;
     const int bh = blockIdx.x / geo.filter_blocks_per_head;
     const int fc = blockIdx.x % geo.filter_blocks_per_head;
-
-    if ((a.mode == MODE_REFRESH || a.mode == MODE_COLD) && fc == 0) {
-        const int8_t code = a.mode == MODE_REFRESH ? PATH_REFRESH : PATH_COLD;
-        if (tid == 0) {
-            if (a.dbg_path) a.dbg_path[bh] = code;
-            if (a.dbg_rho) a.dbg_rho[bh] = __builtin_nan("");
-            if (a.dbg_ncand) a.dbg_ncand[bh] = 0;
-        }
-        if (a.dbg_ret)
-            for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = -1;
-        if (a.dbg_cand)
-            for (int i = tid; i < a.cand_cap; i += NT) a.dbg_cand[(int64_t)bh * a.cand_cap + i] = -1;
-    }
     if (a.mode == MODE_SELECT && w.path[bh] == PATH_REUSE) return;
 
     // The bin b* that holds the kn-th largest score: the largest b with
@@ -773,7 +738,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
 #pragma unroll
         for (int j = 0; j < 4; ++j) c[j] = hist[kHistBins - 1 - 4 * tid - j];
         uint32_t tot = c[0] + c[1] + c[2] + c[3], all;
-        uint32_t above = block_excl_scan<NT>(tot, sm.hist, &all);
+        uint32_t above = block_excl_scan<NT>(tot, s_red, &all);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             if (above < kn && above + c[j] >= kn) s_bstar = (uint32_t)(kHistBins - 1 - 4 * tid - j);
@@ -785,35 +750,65 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
     const float *sc = w.scores + (int64_t)bh * a.max_len;
     uint64_t *sv = w.surv + (int64_t)bh * a.max_len;
     const int64_t i0 = (int64_t)fc * kFilterRows;
+    float s[kFilterRows / NT];
+#pragma unroll
     for (int it = 0; it < kFilterRows / NT; ++it) {
         const int64_t i = i0 + (int64_t)it * NT + tid;
-        float s = 0.0f;
-        bool keep = false;
-        if (i < a.len) {
-            s = sc[i];
-            keep = ord_key(s) >= kmin;
-        }
+        s[it] = i < a.len ? sc[i] : 0.0f;
+    }
+#pragma unroll
+    for (int it = 0; it < kFilterRows / NT; ++it) {
+        const int64_t i = i0 + (int64_t)it * NT + tid;
+        const bool keep = i < a.len && ord_key(s[it]) >= kmin;
         const uint64_t m = __ballot(keep);
         if (m) {
             const int lane = tid & 63;
+            const int leader = __ffsll((unsigned long long)m) - 1;
             uint32_t base = 0;
-            if (lane == __ffsll((unsigned long long)m) - 1)
-                base = atomicAdd(&w.surv_count[bh], (uint32_t)__popcll(m));
-            base = __shfl(base, __ffsll((unsigned long long)m) - 1);
+            if (lane == leader) base = atomicAdd(&w.surv_count[bh], (uint32_t)__popcll(m));
+            base = __shfl(base, leader);
             const uint32_t off = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-            if (keep) sv[base + off] = rank_of(s, (uint32_t)i);
+            if (keep) sv[base + off] = rank_of(s[it], (uint32_t)i);
         }
     }
+}
 
-    if (!arrive_last(&w.ctr_filter[bh], (uint32_t)geo.filter_blocks_per_head, &s_flag)) return;
-    if (tid == 0) {
-        s_n = atomicAdd(&w.surv_count[bh], 0u);
-        w.surv_count[bh] = 0u;
+// ---------------------------------------------------------------------------
+// k_final: one block per query head
+// ---------------------------------------------------------------------------
+
+template <typename T, int D>
+__global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w, Geometry geo)
+{
+    constexpr int NT = kFinalThreads;
+    __shared__ FinalSmem<D, NT> sm;
+    const int tid = threadIdx.x;
+    const int bh = blockIdx.x;
+    (void)geo;
+
+    if (a.mode == MODE_REFRESH || a.mode == MODE_COLD) {
+        const int8_t code = a.mode == MODE_REFRESH ? PATH_REFRESH : PATH_COLD;
+        if (tid == 0) {
+            if (a.dbg_path) a.dbg_path[bh] = code;
+            if (a.dbg_rho) a.dbg_rho[bh] = __builtin_nan("");
+            if (a.dbg_ncand) a.dbg_ncand[bh] = 0;
+        }
+        if (a.dbg_ret)
+            for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = -1;
+        if (a.dbg_cand)
+            for (int i = tid; i < a.cand_cap; i += NT) a.dbg_cand[(int64_t)bh * a.cand_cap + i] = -1;
     }
-    for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)bh * kHistBins + i] = 0u;
-    __syncthreads();
-    finalize_head<T, D, NT>(a, w, bh, sv, (int)s_n, sm);
+    const bool reuse = a.mode == MODE_SELECT && w.path[bh] == PATH_REUSE;
+    if (reuse) {
+        finalize_head<T, D, NT>(a, w, bh, w.cand_ent + (int64_t)bh * a.cand_cap, w.n_cand[bh], sm);
+    } else {
+        const int n = (int)w.surv_count[bh];
+        finalize_head<T, D, NT>(a, w, bh, w.surv + (int64_t)bh * a.max_len, n, sm);
+        // Leave the exact-path workspace zeroed for the next launch.
+        for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)bh * kHistBins + i] = 0u;
+        if (tid == 0) w.surv_count[bh] = 0u;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -829,8 +824,8 @@ bool shape_supported(int dtype, int d, int g)
 template <typename T, int D>
 static hipError_t select_impl(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
 {
-    dim3 grid((unsigned)(a.B * a.Hq * geo.select_blocks_per_head));
-    hipLaunchKernelGGL((k_select<T, D>), grid, dim3(kSelectThreads), 0, s, a, w, geo);
+    hipLaunchKernelGGL((k_select<T, D>), dim3((unsigned)(a.B * a.Hq)), dim3(kSelectThreads), 0, s,
+                       a, w, geo);
     return hipGetLastError();
 }
 
@@ -843,11 +838,18 @@ static hipError_t score_impl(const StepArgs &a, const Ws &w, const Geometry &geo
     return hipGetLastError();
 }
 
-template <typename T, int D>
 static hipError_t filter_impl(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
 {
     dim3 grid((unsigned)(a.B * a.Hq * geo.filter_blocks_per_head));
-    hipLaunchKernelGGL((k_filter<T, D>), grid, dim3(kScoreThreads), 0, s, a, w, geo);
+    hipLaunchKernelGGL(k_filter, grid, dim3(kScoreThreads), 0, s, a, w, geo);
+    return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t final_impl(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
+{
+    hipLaunchKernelGGL((k_final<T, D>), dim3((unsigned)(a.B * a.Hq)), dim3(kFinalThreads), 0, s,
+                       a, w, geo);
     return hipGetLastError();
 }
 
@@ -857,9 +859,9 @@ static hipError_t select_d(const StepArgs &a, const Ws &w, const Geometry &geo, 
     return a.D == 64 ? select_impl<T, 64>(a, w, geo, s) : select_impl<T, 128>(a, w, geo, s);
 }
 template <typename T>
-static hipError_t filter_d(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
+static hipError_t final_d(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
 {
-    return a.D == 64 ? filter_impl<T, 64>(a, w, geo, s) : filter_impl<T, 128>(a, w, geo, s);
+    return a.D == 64 ? final_impl<T, 64>(a, w, geo, s) : final_impl<T, 128>(a, w, geo, s);
 }
 template <typename T, int D>
 static hipError_t score_g(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
@@ -890,7 +892,13 @@ hipError_t launch_score(int dtype, const StepArgs &a, const Ws &w, const Geometr
 hipError_t launch_filter(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
                          hipStream_t s)
 {
-    return dtype == 1 ? filter_d<uint16_t>(a, w, geo, s) : filter_d<float>(a, w, geo, s);
+    (void)dtype;
+    return filter_impl(a, w, geo, s);
+}
+hipError_t launch_final(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
+                        hipStream_t s)
+{
+    return dtype == 1 ? final_d<uint16_t>(a, w, geo, s) : final_d<float>(a, w, geo, s);
 }
 
 }  // namespace retopk
