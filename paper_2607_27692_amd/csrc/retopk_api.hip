@@ -16,9 +16,9 @@ namespace {
 
 constexpr int kProfileMaxLaunches = 65536;
 constexpr int kNumKernels = 4;
-const char *const kKernelNames[kNumKernels] = {"retopk_select", "retopk_score", "retopk_filter",
+const char *const kKernelNames[kNumKernels] = {"retopk_sim", "retopk_score", "retopk_filter",
                                                "retopk_final"};
-enum { KID_SELECT = 0, KID_SCORE = 1, KID_FILTER = 2, KID_FINAL = 3 };
+enum { KID_SIM = 0, KID_SCORE = 1, KID_FILTER = 2, KID_FINAL = 3 };
 
 }  // namespace
 
@@ -58,6 +58,7 @@ retopk_status validate_config(const retopk_config *c)
     if (c->dtype != RETOPK_F32 && c->dtype != RETOPK_BF16) return RETOPK_ERR_ARG;
     if (c->head_dim < 1) return RETOPK_ERR_ARG;
     if (c->max_len < 1 || c->max_len >= ((int64_t)1 << 31)) return RETOPK_ERR_ARG;
+    if (c->max_len > kMaxLen) return RETOPK_ERR_UNSUPPORTED;
     if (c->k < 1 || c->cache_cap < 0 || c->r < 1 || c->window < 0 || c->refresh < 0)
         return RETOPK_ERR_ARG;
     if (!std::isfinite(c->tau)) return RETOPK_ERR_ARG;
@@ -69,6 +70,7 @@ retopk_status validate_config(const retopk_config *c)
 }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 template <typename T>
 retopk_status alloc(retopk_handle h, T **out, size_t count)
@@ -101,19 +103,20 @@ StepArgs base_args(const retopk_handle_s *h)
     a.R = c.r;
     a.W = c.window;
     a.cand_cap = h->cand_cap;
+    a.n_regions = (int)ceil_div(c.max_len, kFilterRows);
+    a.row_stride = (int64_t)a.n_regions * kFilterRows;
     a.tau = c.tau;
     a.inv_sqrt_d = h->inv_sqrt_d;
     a.q_head_stride = c.head_dim;
     return a;
 }
 
-int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
-
-// Rows per scan block: about 128 blocks per (b, KV head), 256..4096 rows, a
-// multiple of the 256 rows one block pass covers.
+// Rows per scan block: about 256 blocks per (b, KV head), so that one KV group's
+// scan alone spreads over every CU; 256..4096 rows, a multiple of the 256 rows
+// one block pass covers.
 int scan_chunk_rows(int64_t len)
 {
-    int64_t want = ceil_div(len, 128);
+    int64_t want = ceil_div(len, 256);
     int64_t rows = 256;
     while (rows < want && rows < 4096) rows <<= 1;
     return (int)rows;
@@ -125,31 +128,29 @@ Geometry make_geometry(const retopk_handle_s *h, int64_t len, int mode)
     Geometry g{};
     g.scan_chunk_rows = scan_chunk_rows(len);
     g.scan_blocks = (int)((int64_t)c.batch * c.n_kv_heads * ceil_div(len, g.scan_chunk_rows));
-    g.cand_blocks_per_head = mode == MODE_SELECT ? (int)ceil_div(h->cand_cap, kCandRows) : 0;
+    g.cand_blocks = mode == MODE_SELECT ? (int)(heads_of(c) * kCandRanges) : 0;
     g.filter_blocks_per_head = (int)ceil_div(len, kFilterRows);
     return g;
 }
 
-retopk_status record(retopk_handle h, hipStream_t s, int kid, bool begin)
+// Event pair for the next launch of kernel `kid` when profiling is on.
+retopk_status timing_for(retopk_handle h, int kid, Timing *tm)
 {
+    *tm = Timing{};
     if (!h->prof) return RETOPK_OK;
-    if (begin) {
-        if (h->ev_used / 2 >= (size_t)kProfileMaxLaunches) {
-            h->prof_overflow = true;
-            return RETOPK_OK;
-        }
-        while (h->ev.size() < h->ev_used + 2) {
-            hipEvent_t e;
-            if (hipEventCreate(&e) != hipSuccess) return RETOPK_ERR_HIP;
-            h->ev.push_back(e);
-        }
-        if (hipEventRecord(h->ev[h->ev_used], s) != hipSuccess) return RETOPK_ERR_HIP;
-        h->ev_kernel.push_back(kid);
-    } else {
-        if (h->ev_kernel.size() * 2 != h->ev_used + 2) return RETOPK_OK;   // begin was dropped
-        if (hipEventRecord(h->ev[h->ev_used + 1], s) != hipSuccess) return RETOPK_ERR_HIP;
-        h->ev_used += 2;
+    if (h->ev_used / 2 >= (size_t)kProfileMaxLaunches) {
+        h->prof_overflow = true;
+        return RETOPK_OK;
     }
+    while (h->ev.size() < h->ev_used + 2) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return RETOPK_ERR_HIP;
+        h->ev.push_back(e);
+    }
+    tm->start = h->ev[h->ev_used];
+    tm->stop = h->ev[h->ev_used + 1];
+    h->ev_kernel.push_back(kid);
+    h->ev_used += 2;
     return RETOPK_OK;
 }
 
@@ -164,21 +165,18 @@ retopk_status run_step(retopk_handle h, const StepArgs &a, int mode, hipStream_t
 {
     const Geometry geo = make_geometry(h, a.len, mode);
     const int dt = h->cfg.dtype;
+    Timing tm;
     retopk_status st;
     if (mode == MODE_SELECT) {
-        if ((st = record(h, s, KID_SELECT, true)) != RETOPK_OK) return st;
-        if (launch_select(dt, a, h->w, geo, s) != hipSuccess) return fail(h);
-        if ((st = record(h, s, KID_SELECT, false)) != RETOPK_OK) return st;
+        if ((st = timing_for(h, KID_SIM, &tm)) != RETOPK_OK) return st;
+        if (launch_sim(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
     }
-    if ((st = record(h, s, KID_SCORE, true)) != RETOPK_OK) return st;
-    if (launch_score(dt, a, h->w, geo, s) != hipSuccess) return fail(h);
-    if ((st = record(h, s, KID_SCORE, false)) != RETOPK_OK) return st;
-    if ((st = record(h, s, KID_FILTER, true)) != RETOPK_OK) return st;
-    if (launch_filter(dt, a, h->w, geo, s) != hipSuccess) return fail(h);
-    if ((st = record(h, s, KID_FILTER, false)) != RETOPK_OK) return st;
-    if ((st = record(h, s, KID_FINAL, true)) != RETOPK_OK) return st;
-    if (launch_final(dt, a, h->w, geo, s) != hipSuccess) return fail(h);
-    if ((st = record(h, s, KID_FINAL, false)) != RETOPK_OK) return st;
+    if ((st = timing_for(h, KID_SCORE, &tm)) != RETOPK_OK) return st;
+    if (launch_score(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
+    if ((st = timing_for(h, KID_FILTER, &tm)) != RETOPK_OK) return st;
+    if (launch_filter(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
+    if ((st = timing_for(h, KID_FINAL, &tm)) != RETOPK_OK) return st;
+    if (launch_final(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
     return RETOPK_OK;
 }
 
@@ -230,17 +228,21 @@ retopk_status retopk_create(const retopk_config *cfg, retopk_handle *out)
     const int64_t BH = heads_of(*cfg);
     const int64_t C = cfg->cache_cap, D = cfg->head_dim, K = cfg->k, L = cfg->max_len;
     Ws &w = h->w;
+    const int64_t NR = ceil_div(L, kFilterRows), RS = NR * kFilterRows;
+    const int64_t NSB = kMaxCache / kSimSlots;
     if ((st = alloc(h, &w.qbar, (size_t)(BH * C * D))) != RETOPK_OK ||
         (st = alloc(h, &w.supp, (size_t)(BH * C * K))) != RETOPK_OK ||
         (st = alloc(h, &w.cnt, (size_t)(BH * C))) != RETOPK_OK ||
-        (st = alloc(h, &w.scores, (size_t)(BH * L))) != RETOPK_OK ||
-        (st = alloc(h, &w.surv, (size_t)(BH * L))) != RETOPK_OK ||
-        (st = alloc(h, &w.hist, (size_t)(BH * kHistBins))) != RETOPK_OK ||
-        (st = alloc(h, &w.cand, (size_t)(BH * h->cand_cap))) != RETOPK_OK ||
-        (st = alloc(h, &w.cand_ent, (size_t)(BH * h->cand_cap))) != RETOPK_OK ||
+        (st = alloc(h, &w.rho, (size_t)(BH * C))) != RETOPK_OK ||
+        (st = alloc(h, &w.rho_bmax, (size_t)(BH * NSB))) != RETOPK_OK ||
+        (st = alloc(h, &w.qbar_cur, (size_t)(BH * D))) != RETOPK_OK ||
         (st = alloc(h, &w.path, (size_t)BH)) != RETOPK_OK ||
-        (st = alloc(h, &w.n_cand, (size_t)BH)) != RETOPK_OK ||
-        (st = alloc(h, &w.surv_count, (size_t)BH)) != RETOPK_OK ||
+        (st = alloc(h, &w.scores, (size_t)(BH * RS))) != RETOPK_OK ||
+        (st = alloc(h, &w.hist, (size_t)(BH * kHistBins))) != RETOPK_OK ||
+        (st = alloc(h, &w.surv, (size_t)(BH * RS))) != RETOPK_OK ||
+        (st = alloc(h, &w.surv_cnt, (size_t)(BH * NR))) != RETOPK_OK ||
+        (st = alloc(h, &w.cand_ent, (size_t)(BH * kCandRanges * h->cand_cap))) != RETOPK_OK ||
+        (st = alloc(h, &w.cand_cnt, (size_t)(BH * kCandRanges))) != RETOPK_OK ||
         (st = alloc(h, &w.stats, (size_t)STAT_COUNT)) != RETOPK_OK) {
         retopk_destroy(h);
         return st;

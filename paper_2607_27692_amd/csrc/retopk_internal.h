@@ -12,17 +12,22 @@ namespace retopk {
 constexpr int kHistBins = 2048;
 constexpr int kHistShift = 21;
 
+constexpr int kSimThreads = 256;      // k_sim: 64 cached slots per block
+constexpr int kSimSlots = 64;
 constexpr int kScoreThreads = 512;    // k_score and k_filter blocks
-constexpr int kSelectThreads = 1024;  // k_select: one block per query head
-constexpr int kFinalThreads = 1024;   // k_final: one block per query head
+constexpr int kFinalThreads = 512;    // k_final blocks
+constexpr int kFinalSlices = 4;       // k_final blocks per head (one d-slice of V each)
 constexpr int kScanRowsPerIter = 128; // 8 waves x 16 rows
-constexpr int kCandRows = 512;        // candidates scored per k_score candidate block
+constexpr int kCandRanges = 16;       // index ranges (k_score blocks) per reuse head
+constexpr int kCandList = 2048;       // candidates gathered per round in one range block
+constexpr int kSegWords = 2048;       // union bitmap segment: 65536 indices
 constexpr int kFilterRows = 4096;     // scores filtered per k_filter block
-constexpr int kBitmapWords = 8192;    // union bitmap segment: 262144 indices
-constexpr int kEntCache = 6144;       // final-stage entries staged in LDS
+constexpr int kEntCache = 8704;       // final-stage entries staged in LDS
+constexpr int kMaxRegions = 4096;     // filter regions per head (max_len <= 16M)
 constexpr int kMaxK = 2048;
 constexpr int kMaxR = 32;
 constexpr int kMaxCache = 4096;
+constexpr int64_t kMaxLen = (int64_t)kMaxRegions * kFilterRows;
 
 // Step modes.  SELECT runs the per-head path rule on the device; the others take
 // the exact path for every head.
@@ -50,14 +55,16 @@ struct Ws {
     int32_t *supp;        // [BH, C, K], ascending, -1 padded
     int32_t *cnt;         // [BH, C]
     // per-step workspaces
-    float *scores;        // [BH, max_len] full-history scores of exact heads
-    uint64_t *surv;       // [BH, max_len] surviving (rank key) entries of exact heads
+    double *rho;          // [BH, C] cosine similarities of this step
+    double *rho_bmax;     // [BH, kMaxCache / kSimSlots] per-k_sim-block maxima of rho
+    float *qbar_cur;      // [BH, d] q_bar of this step
+    int8_t *path;         // [BH] path of this step
+    float *scores;        // [BH, row_stride] full-history scores of exact heads
     uint32_t *hist;       // [BH, kHistBins] score histogram (zero between steps)
-    int32_t *cand;        // [BH, cand_cap] candidate set, ascending
-    uint64_t *cand_ent;   // [BH, cand_cap] candidate rank keys
-    int8_t *path;         // [BH]
-    int32_t *n_cand;      // [BH]
-    uint32_t *surv_count; // [BH] survivors appended by k_filter (zero between steps)
+    uint64_t *surv;       // [BH, row_stride] surviving rank entries, region f at f*kFilterRows
+    uint32_t *surv_cnt;   // [BH, n_regions] entries in each filter region
+    uint64_t *cand_ent;   // [BH, kCandRanges, cand_cap] candidate rank entries per range
+    uint32_t *cand_cnt;   // [BH, kCandRanges]
     unsigned long long *stats;  // [STAT_COUNT]
 };
 
@@ -67,6 +74,8 @@ struct StepArgs {
     int64_t max_len;
     int K, M, R, W;
     int cand_cap;
+    int n_regions;             // ceil(max_len / kFilterRows): surv_cnt row length
+    int64_t row_stride;        // n_regions * kFilterRows: row length of scores and surv
     float tau;
     float inv_sqrt_d;          // fl32(1 / sqrt(d))
     int mode;
@@ -91,20 +100,26 @@ struct StepArgs {
 // Launch geometry chosen on the host.
 struct Geometry {
     int scan_chunk_rows;
-    int scan_blocks;           // B * Hkv * chunks (0 when the mode never scans)
-    int cand_blocks_per_head;  // 0 outside MODE_SELECT
+    int scan_blocks;           // B * Hkv * chunks
+    int cand_blocks;           // B * Hq * kCandRanges in MODE_SELECT, else 0
     int filter_blocks_per_head;
 };
 
+// Optional start/stop events attached to one kernel dispatch (both null: none).
+struct Timing {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+
 // Launchers (retopk_kernels.hip).  dtype: 0 = f32, 1 = bf16.
-hipError_t launch_select(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                         hipStream_t s);
+hipError_t launch_sim(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
+                      hipStream_t s, const Timing &tm);
 hipError_t launch_score(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                        hipStream_t s);
+                        hipStream_t s, const Timing &tm);
 hipError_t launch_filter(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                         hipStream_t s);
+                         hipStream_t s, const Timing &tm);
 hipError_t launch_final(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                        hipStream_t s);
+                        hipStream_t s, const Timing &tm);
 bool shape_supported(int dtype, int d, int g);
 
 }  // namespace retopk

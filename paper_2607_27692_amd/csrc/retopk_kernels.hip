@@ -1,27 +1,31 @@
 // retopk_kernels.hip -- gfx950 (CDNA4) kernels of the ReTopK decode step.
 //
-// One decode step is four launches on the caller's stream:
-//   k_select  one block per query head: q_bar, cosine similarity to the cached
-//             queries (Eq. 6), rho_max, Top-R (Eq. 7), the path rule (Eq. 13) and,
-//             on reuse, the candidate set of Eq. 8-9 (union through an LDS bitmap,
-//             emitted in ascending order).
-//   k_score   full-history QK scan of every KV group that has an exact head
-//             (Eq. 4; one key row load serves the G query heads of the group) with
-//             a per-head score histogram, plus gathered QK on the candidate sets
-//             of reuse heads (Eq. 10).
-//   k_filter  for every exact head: keep the scores at or above the histogram bin
-//             that holds the K-th largest.
-//   k_final   one block per query head: Top-K over the head's candidates (Eq. 11)
-//             or surviving scores (Eq. 1), Softmax-V (Eq. 12), outputs, and the
-//             cache insert of Sec. 3.4.
+// One decode step is four launches on the caller's stream, and blocks never wait
+// on each other inside a launch (every hand-over is a kernel boundary):
+//   k_sim     cosine similarity of q_bar to every cached query (Eq. 5, Eq. 6),
+//             64 cache slots per block, plus per-block maxima of rho.
+//   k_score   (a) full-history QK scan of every KV group with an exact head
+//             (Eq. 4): one key-row load serves the G query heads of the group, and
+//             each block adds its scores to a per-head histogram;
+//             (b) for every query head, kCandRanges blocks each own one index range:
+//             they apply the path rule (Eq. 13), take the Top-R cache entries
+//             (Eq. 7), form the range's part of the candidate set (Eq. 8-9) through
+//             an LDS bitmap and score those keys (Eq. 10).
+//   k_filter  per exact head, the scores at or above the histogram bin that holds
+//             the K-th largest, compacted in index order.
+//   k_final   kFinalSlices blocks per head: each selects the Top-K of the head's
+//             candidates (Eq. 11) or surviving scores (Eq. 1) by radix select on
+//             64-bit ranks, then aggregates one slice of the head dimension of
+//             Softmax-V (Eq. 12); slice 0 writes the support and inserts into the
+//             cache (Sec. 3.4).
 // Exact Top-K attention alone is k_score (scan only) + k_filter + k_final.
-// Blocks never wait on each other inside a launch: every hand-over between
-// blocks goes through a kernel boundary.
 //
 // Ranking is on the fp32 scaled score fl32(q.k) * fl32(1/sqrt d) with ties to the
-// lower index: every candidate carries a 64-bit rank (score key << 32 | ~index)
-// and selection is a radix select over those distinct ranks.
+// lower index: every entry carries a 64-bit rank (score key << 32 | ~index), and
+// ranks are distinct.
 #include "retopk_internal.h"
+
+#include <hip/hip_ext.h>
 
 namespace retopk {
 
@@ -199,14 +203,41 @@ template <> struct Dot<float> {
     }
 };
 
-template <int G>
-__device__ __forceinline__ float pick(const float (&acc)[G], int j)
+// Reduce-scatter inside a quad: lane p of the quad holds partial sums a0..a3 of
+// four dot products; on return it holds the full (4-lane) sum of dot product p.
+// Two butterfly steps: at each one a lane keeps the half of its values whose
+// index bit matches its own lane bit and sends the other half to its partner.
+__device__ __forceinline__ float quad_transpose_sum(float a0, float a1, float a2, float a3, int p)
 {
-    float r = acc[0];
-#pragma unroll
-    for (int t = 1; t < G; ++t)
-        if (t == j) r = acc[t];
-    return r;
+    const bool b0 = (p & 1) != 0, b1 = (p & 2) != 0;
+    const float keep0 = b0 ? a1 : a0, send0 = b0 ? a0 : a1;
+    const float keep1 = b0 ? a3 : a2, send1 = b0 ? a2 : a3;
+    const float r0 = keep0 + dpp_f32<kQuadXor1>(send0);   // dot 0 + b0
+    const float r1 = keep1 + dpp_f32<kQuadXor1>(send1);   // dot 2 + b0
+    const float keep = b1 ? r1 : r0, send = b1 ? r0 : r1;
+    return keep + dpp_f32<kQuadXor2>(send);                // dot 2*b1 + b0
+}
+
+// Full scores of a G-head group after each lane of a quad accumulated its quarter
+// of every row: lane p returns the scores of heads p and p + 4 (when they exist).
+template <int G>
+__device__ __forceinline__ void group_scores(const float (&acc)[G], int p, float &s_lo, float &s_hi)
+{
+    if constexpr (G == 1) {
+        s_lo = quad_sum(acc[0]);
+        s_hi = 0.0f;
+    } else if constexpr (G == 2) {
+        const bool b0 = (p & 1) != 0;
+        const float r = (b0 ? acc[1] : acc[0]) + dpp_f32<kQuadXor1>(b0 ? acc[0] : acc[1]);
+        s_lo = r + dpp_f32<kQuadXor2>(r);
+        s_hi = 0.0f;
+    } else if constexpr (G == 4) {
+        s_lo = quad_transpose_sum(acc[0], acc[1], acc[2], acc[3], p);
+        s_hi = 0.0f;
+    } else {
+        s_lo = quad_transpose_sum(acc[0], acc[1], acc[2], acc[3], p);
+        s_hi = quad_transpose_sum(acc[4], acc[5], acc[6], acc[7], p);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -225,379 +256,101 @@ __device__ void block_qbar(const T *q, float *s_qbar, double *red)
     __syncthreads();
 }
 
-// ---------------------------------------------------------------------------
-// Final stage of one head: Top-K over rank entries, Softmax-V, outputs, insert.
-// ---------------------------------------------------------------------------
-
-template <int D, int NT>
-struct FinalSmem {
-    uint64_t ent[kEntCache];  // the head's entries, when they fit
-    uint64_t sel[kMaxK];      // selected (index << 32 | score key), sorted by index
-    float wgt[kMaxK];
-    float part[NT / 64][D];
-    uint32_t hist[256];
-    float qbar[D];
-    double red64[NT / 64];
-    float red32[NT / 64];
-    uint32_t found_digit, found_above, found_cnt, count;
-};
-
-// Selects the top min(K, n) of src[0..n) (distinct 64-bit ranks, larger is
-// better), then sorts them by index.  Returns the number selected.
-template <int D, int NT>
-__device__ int select_topk(const uint64_t *src, int n, int K, FinalSmem<D, NT> &sm)
-{
-    const int tid = threadIdx.x;
-    uint64_t prefix = 0, mask = 0;
-    const bool all = n <= K;
-    if (!all) {
-        uint32_t k_rem = (uint32_t)K;
-        // Radix select on 8-bit digits, most significant first: after each pass the
-        // selected set is {rank : (rank & mask) > prefix} plus k_rem entries that
-        // still match prefix under mask.
-        for (int shift = 56; shift >= 0; shift -= 8) {
-            for (int i = tid; i < 256; i += NT) sm.hist[i] = 0;
-            __syncthreads();
-            for (int i = tid; i < n; i += NT) {
-                uint64_t e = src[i];
-                if ((e & mask) == prefix) atomicAdd(&sm.hist[(e >> shift) & 255u], 1u);
-            }
-            __syncthreads();
-            if (tid < 64) {
-                // lane l covers digits 255-4l, 254-4l, 253-4l, 252-4l (descending)
-                uint32_t c[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) c[j] = sm.hist[255 - 4 * tid - j];
-                uint32_t tot = c[0] + c[1] + c[2] + c[3];
-                uint32_t above = wave_incl_scan(tot) - tot;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (above < k_rem && above + c[j] >= k_rem) {
-                        sm.found_digit = 255u - 4u * tid - j;
-                        sm.found_above = above;
-                        sm.found_cnt = c[j];
-                    }
-                    above += c[j];
-                }
-            }
-            __syncthreads();
-            const uint32_t dgt = sm.found_digit;
-            k_rem -= sm.found_above;
-            prefix |= (uint64_t)dgt << shift;
-            mask |= (uint64_t)0xFFu << shift;
-            const bool done = sm.found_cnt == k_rem;
-            __syncthreads();
-            if (done) break;
-        }
-    }
-    const int kn = all ? n : K;
-    if (tid == 0) sm.count = 0;
-    __syncthreads();
-    for (int i = tid; i < n; i += NT) {
-        uint64_t e = src[i];
-        if (all || (e & mask) >= prefix) {
-            uint32_t pos = atomicAdd(&sm.count, 1u);
-            if (pos < (uint32_t)kMaxK) sm.sel[pos] = ((uint64_t)rank_index(e) << 32) | rank_key(e);
-        }
-    }
-    int kp = 1;
-    while (kp < kn) kp <<= 1;
-    __syncthreads();
-    for (int i = kn + tid; i < kp; i += NT) sm.sel[i] = ~0ull;
-    __syncthreads();
-    // Bitonic sort (ascending) of sel[0..kp) -> ascending index order.
-    for (int k2 = 2; k2 <= kp; k2 <<= 1) {
-        for (int j = k2 >> 1; j > 0; j >>= 1) {
-            for (int i = tid; i < kp; i += NT) {
-                int ixj = i ^ j;
-                if (ixj > i) {
-                    uint64_t x = sm.sel[i], y = sm.sel[ixj];
-                    bool up = (i & k2) == 0;
-                    if ((x > y) == up) {
-                        sm.sel[i] = y;
-                        sm.sel[ixj] = x;
-                    }
-                }
-            }
-            __syncthreads();
-        }
-    }
-    return kn;
-}
-
-// Top-K of ents[0..n), Softmax-V over the selected rows (Eq. 12), sel output and
-// cache insert.
-template <typename T, int D, int NT>
-__device__ void finalize_head(const StepArgs &a, const Ws &w, int bh, const uint64_t *ents,
-                              int n, FinalSmem<D, NT> &sm)
-{
-    using R = RowT<T, D>;
-    constexpr int LPR = R::kBytes / 16;   // lanes per row for 16-byte loads
-    constexpr int RPW = 64 / LPR;         // rows per wave instruction
-    constexpr int EPV = R::kEPV;
-    constexpr int NW = NT / 64;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
-
-    const uint64_t *src = ents;
-    if (n <= kEntCache) {
-        for (int i = tid; i < n; i += NT) sm.ent[i] = ents[i];
-        __syncthreads();
-        src = sm.ent;
-    }
-    const int kn = select_topk<D, NT>(src, n, a.K, sm);
-
-    if (a.out != nullptr && a.mode != MODE_PREFILL) {
-        float mx = -INFINITY;
-        for (int t = tid; t < kn; t += NT) mx = fmaxf(mx, key_score((uint32_t)sm.sel[t]));
-        mx = block_reduce<NT>(mx, sm.red32, [](float x, float y) { return fmaxf(x, y); });
-        float lsum = 0.0f;
-        for (int t = tid; t < kn; t += NT) {
-            float wt = expf(key_score((uint32_t)sm.sel[t]) - mx);
-            sm.wgt[t] = wt;
-            lsum += wt;
-        }
-        lsum = block_reduce<NT>(lsum, sm.red32, [](float x, float y) { return x + y; });
-        // block_reduce ends with a barrier, so wgt[] is visible here.
-        const T *vbase = (const T *)a.v + ((int64_t)b * a.Hkv + g) * a.max_len * D;
-        const int sub = lane / LPR, vl = lane % LPR;
-        float acc[EPV];
-#pragma unroll
-        for (int e = 0; e < EPV; ++e) acc[e] = 0.0f;
-#pragma unroll 8
-        for (int t = wave * RPW + sub; t < kn; t += NW * RPW) {
-            uint32_t idx = (uint32_t)(sm.sel[t] >> 32);
-            uint4 raw = ((const uint4 *)(vbase + (int64_t)idx * D))[vl];
-            Dot<T>::axpy(raw, sm.wgt[t], acc);
-        }
-#pragma unroll
-        for (int o = LPR; o < 64; o <<= 1)
-#pragma unroll
-            for (int e = 0; e < EPV; ++e) acc[e] += __shfl_xor(acc[e], o);
-        if (sub == 0)
-#pragma unroll
-            for (int e = 0; e < EPV; ++e) sm.part[wave][vl * EPV + e] = acc[e];
-        __syncthreads();
-        if (tid < D) {
-            float o = 0.0f;
-#pragma unroll
-            for (int ww = 0; ww < NW; ++ww) o += sm.part[ww][tid];
-            a.out[(int64_t)bh * D + tid] = kn > 0 ? o / lsum : 0.0f;
-        }
-    }
-    if (a.sel != nullptr && a.mode != MODE_PREFILL) {
-        for (int t = tid; t < a.K; t += NT)
-            a.sel[(int64_t)bh * a.K + t] = t < kn ? (int32_t)(sm.sel[t] >> 32) : -1;
-    }
-    if (a.do_insert) {
-        const T *q = (const T *)a.q + (int64_t)bh * a.q_head_stride;
-        block_qbar<T, D, NT>(q, sm.qbar, sm.red64);
-        const int64_t e = (int64_t)bh * a.M + a.insert_slot;
-        for (int t = tid; t < D; t += NT) w.qbar[e * D + t] = sm.qbar[t];
-        for (int t = tid; t < a.K; t += NT)
-            w.supp[e * a.K + t] = t < kn ? (int32_t)(sm.sel[t] >> 32) : -1;
-        if (tid == 0) w.cnt[e] = kn;
-    }
-}
 
 // ---------------------------------------------------------------------------
-// k_select: one block per query head
+// k_sim: rho for 64 cache slots per block (Eq. 6)
 // ---------------------------------------------------------------------------
-
-template <int D>
-struct SelectSmem {
-    uint32_t bitmap[kBitmapWords];
-    double rho[kMaxCache];
-    float qbar[D];
-    double red64[kSelectThreads / 64];
-    uint32_t red32[kSelectThreads / 64];
-    double best_rho[kSelectThreads / 64];
-    int32_t best_age[kSelectThreads / 64];
-    int32_t best_slot[kSelectThreads / 64];
-    int32_t ret[kMaxR];
-    uint8_t taken[kMaxCache];
-};
-
-__device__ __forceinline__ bool better(double ra, int aa, double rb, int ab)
-{
-    return ra > rb || (ra == rb && aa < ab);
-}
 
 template <typename T, int D>
-__global__ __launch_bounds__(kSelectThreads) void k_select(StepArgs a, Ws w, Geometry geo)
+__global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
 {
-    constexpr int NT = kSelectThreads;
-    constexpr int NW = NT / 64;
-    __shared__ SelectSmem<D> sm;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bh = blockIdx.x;
+    constexpr int NT = kSimThreads;
+    __shared__ float s_qbar[D];
+    __shared__ double s_red[NT / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3;
     const int M = a.M;
+    const int nsb = (M + kSimSlots - 1) / kSimSlots;
+    const int bh = blockIdx.x / nsb, sb = blockIdx.x % nsb;
     const int n_valid = (int)(a.n_ins < (int64_t)M ? a.n_ins : (int64_t)M);
-    const T *q = (const T *)a.q + (int64_t)bh * a.q_head_stride;
 
-    block_qbar<T, D, NT>(q, sm.qbar, sm.red64);
+    block_qbar<T, D, NT>((const T *)a.q + (int64_t)bh * a.q_head_stride, s_qbar, s_red);
+    if (sb == 0)
+        for (int t = tid; t < D; t += NT) w.qbar_cur[(int64_t)bh * D + t] = s_qbar[t];
 
-    // Eq. 6: 16 slots per wave pass, 4 lanes per cached row.
-    {
-        const int p = lane & 3;
-        const float4 *cache = (const float4 *)(w.qbar + (int64_t)bh * M * D);
-        for (int base = 0; base < n_valid; base += NW * 16) {
-            const int slot = base + wave * 16 + (lane >> 2);
-            float4 c[D / 16];
+    // 16 slots per wave, 4 lanes per cached row of D floats.
+    const int slot = sb * kSimSlots + wave * 16 + (lane >> 2);
+    const float4 *crow = (const float4 *)(w.qbar + ((int64_t)bh * M + (slot < n_valid ? slot : 0)) * D);
+    float4 c[D / 16];
 #pragma unroll
-            for (int s = 0; s < D / 16; ++s)
-                c[s] = slot < n_valid ? cache[(int64_t)slot * (D / 4) + s * 4 + p]
-                                      : make_float4(0.f, 0.f, 0.f, 0.f);
-            double acc = 0.0;
+    for (int s = 0; s < D / 16; ++s)
+        c[s] = slot < n_valid ? crow[s * 4 + p] : make_float4(0.f, 0.f, 0.f, 0.f);
+    double acc = 0.0;
 #pragma unroll
-            for (int s = 0; s < D / 16; ++s) {
-                const float *qq = &sm.qbar[(s * 4 + p) * 4];
-                acc += (double)c[s].x * (double)qq[0];
-                acc += (double)c[s].y * (double)qq[1];
-                acc += (double)c[s].z * (double)qq[2];
-                acc += (double)c[s].w * (double)qq[3];
-            }
-            acc = quad_sum(acc);
-            if (slot < n_valid && p == 0) sm.rho[slot] = acc;
-        }
+    for (int s = 0; s < D / 16; ++s) {
+        const float *qq = &s_qbar[(s * 4 + p) * 4];
+        acc += (double)c[s].x * (double)qq[0];
+        acc += (double)c[s].y * (double)qq[1];
+        acc += (double)c[s].z * (double)qq[2];
+        acc += (double)c[s].w * (double)qq[3];
     }
-    __syncthreads();
-
-    double mx = -INFINITY;
-    for (int i = tid; i < n_valid; i += NT) mx = fmax(mx, sm.rho[i]);
-    mx = block_reduce<NT>(mx, sm.red64, [](double x, double y) { return fmax(x, y); });
-
-    // Eq. 13 (no refresh in this mode): exact path iff rho_max < tau.
-    const int8_t path = mx < (double)a.tau ? PATH_FALLBACK : PATH_REUSE;
-    if (tid == 0) {
-        w.path[bh] = path;
-        if (a.dbg_path) a.dbg_path[bh] = path;
-        if (a.dbg_rho) a.dbg_rho[bh] = mx;
-        atomicAdd(&w.stats[path == PATH_REUSE ? STAT_REUSE : STAT_FALLBACK], 1ull);
-    }
-    const int nret = path == PATH_REUSE ? (a.R < n_valid ? a.R : n_valid) : 0;
-
-    // Eq. 7: the nret most similar slots; equal similarity -> newer insertion
-    // (smaller age = (n_ins - 1 - slot) mod C).
-    for (int i = tid; i < n_valid; i += NT) sm.taken[i] = 0;
-    __syncthreads();
-    for (int r = 0; r < nret; ++r) {
-        double br = -INFINITY;
-        int ba = 0x7FFFFFFF, bs = -1;
-        for (int i = tid; i < n_valid; i += NT) {
-            if (sm.taken[i]) continue;
-            int age = (int)(((a.n_ins - 1 - i) % M + M) % M);
-            if (bs < 0 || better(sm.rho[i], age, br, ba)) { br = sm.rho[i]; ba = age; bs = i; }
-        }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            double orr = __shfl_xor(br, o);
-            int oa = __shfl_xor(ba, o), os = __shfl_xor(bs, o);
-            if (os >= 0 && (bs < 0 || better(orr, oa, br, ba))) { br = orr; ba = oa; bs = os; }
-        }
-        if (lane == 0) { sm.best_rho[wave] = br; sm.best_age[wave] = ba; sm.best_slot[wave] = bs; }
-        __syncthreads();
-        if (tid == 0) {
-            double fr = sm.best_rho[0];
-            int fa = sm.best_age[0], fs = sm.best_slot[0];
-            for (int ww = 1; ww < NW; ++ww) {
-                int os = sm.best_slot[ww];
-                if (os >= 0 && (fs < 0 || better(sm.best_rho[ww], sm.best_age[ww], fr, fa))) {
-                    fr = sm.best_rho[ww]; fa = sm.best_age[ww]; fs = os;
-                }
-            }
-            sm.ret[r] = fs;
-            sm.taken[fs] = 1;
-        }
-        __syncthreads();
-    }
-    if (a.dbg_ret)
-        for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = i < nret ? sm.ret[i] : -1;
-
-    int total = 0;
-    if (path == PATH_REUSE) {
-        // Eq. 8-9: union of the retrieved supports and the window [len-W, len),
-        // through a bitmap over index segments; compaction emits ascending order.
-        const int64_t len = a.len;
-        const int64_t w0 = len - a.W > 0 ? len - a.W : 0;
-        int32_t *cand = w.cand + (int64_t)bh * a.cand_cap;
-        int32_t *dcand = a.dbg_cand ? a.dbg_cand + (int64_t)bh * a.cand_cap : nullptr;
-        for (int64_t lo = 0; lo < len; lo += (int64_t)kBitmapWords * 32) {
-            const int64_t hi = (lo + (int64_t)kBitmapWords * 32 < len) ? lo + (int64_t)kBitmapWords * 32 : len;
-            const int nwords = (int)((hi - lo + 31) >> 5);
-            for (int i = tid; i < nwords; i += NT) sm.bitmap[i] = 0u;
-            __syncthreads();
-            for (int r = 0; r < nret; ++r) {
-                const int64_t e = (int64_t)bh * M + sm.ret[r];
-                const int32_t *sp = w.supp + e * a.K;
-                const int c = w.cnt[e];
-                for (int t = tid; t < c; t += NT) {
-                    int64_t x = sp[t];
-                    if (x >= lo && x < hi) atomicOr(&sm.bitmap[(x - lo) >> 5], 1u << ((x - lo) & 31));
-                }
-            }
-            for (int64_t x = (w0 > lo ? w0 : lo) + tid; x < hi; x += NT)
-                atomicOr(&sm.bitmap[(x - lo) >> 5], 1u << ((x - lo) & 31));
-            __syncthreads();
-            const int wpt = (nwords + NT - 1) / NT;
-            const int wb = tid * wpt;
-            const int we = (wb + wpt < nwords) ? wb + wpt : nwords;
-            uint32_t mine = 0;
-            for (int i = wb; i < we; ++i) mine += __popc(sm.bitmap[i]);
-            uint32_t seg_total;
-            uint32_t pos = (uint32_t)total + block_excl_scan<NT>(mine, sm.red32, &seg_total);
-            for (int i = wb; i < we; ++i) {
-                uint32_t bits = sm.bitmap[i];
-                while (bits) {
-                    int bit = __ffs(bits) - 1;
-                    bits &= bits - 1u;
-                    int32_t x = (int32_t)(lo + (int64_t)i * 32 + bit);
-                    cand[pos] = x;
-                    if (dcand) dcand[pos] = x;
-                    ++pos;
-                }
-            }
-            total += (int)seg_total;
-            __syncthreads();
-        }
-        if (tid == 0) {
-            atomicAdd(&w.stats[STAT_CAND_SUM], (unsigned long long)total);
-            atomicMax(&w.stats[STAT_CAND_MAX], (unsigned long long)total);
-        }
-    }
-    if (tid == 0) {
-        w.n_cand[bh] = total;
-        if (a.dbg_ncand) a.dbg_ncand[bh] = total;
-    }
-    if (a.dbg_cand)
-        for (int i = total + tid; i < a.cand_cap; i += NT) a.dbg_cand[(int64_t)bh * a.cand_cap + i] = -1;
+    acc = quad_sum(acc);
+    if (slot < n_valid && p == 0) w.rho[(int64_t)bh * M + slot] = acc;
+    const double bmax = block_reduce<NT>(slot < n_valid ? acc : -INFINITY, s_red,
+                                         [](double x, double y) { return fmax(x, y); });
+    if (tid == 0) w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = bmax;
 }
 
 // ---------------------------------------------------------------------------
-// k_score: full-history scan blocks, then candidate blocks
+// k_score
 // ---------------------------------------------------------------------------
 
+// LDS of k_score: the scan blocks' histograms, or a range block's rho array,
+// which later holds the union bitmap segment and the candidate list.
+template <int G>
+struct ScoreLds {
+    static constexpr int kScan = G * kHistBins * 4;
+    static constexpr int kRho = 8 * kMaxCache;
+    static constexpr int kSeg = kSegWords * 4 + kCandList * 4;
+    static constexpr int kCand = kRho > kSeg ? kRho : kSeg;
+    static constexpr int kBytes = kScan > kCand ? kScan : kCand;
+};
+
+// Scan block: scores of rows [chunk*rows, ...) of KV head (b, g) for the group's
+// exact heads, written to `scores` and counted in the per-head histogram.
 template <typename T, int D, int G>
-__device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, uint32_t *s_hist)
+__device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, unsigned char *lds)
 {
     using R = RowT<T, D>;
+    __shared__ uint32_t s_exmask;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
     const int chunks = geo.scan_blocks / (a.B * a.Hkv);
     const int bg = blockIdx.x / chunks, chunk = blockIdx.x % chunks;
     const int b = bg / a.Hkv, g = bg % a.Hkv;
     const int bh0 = b * a.Hq + g * G;
 
-    uint32_t exmask = 0;
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-        bool ex = a.mode != MODE_SELECT || w.path[bh0 + j] != PATH_REUSE;
-        exmask |= (uint32_t)ex << j;
+    if (tid == 0) {
+        uint32_t m = (1u << G) - 1u;
+        if (a.mode == MODE_SELECT) {
+            // Eq. 13: a head is exact iff rho_max < tau (rho_max from k_sim's block maxima).
+            const int nsb = (a.M + kSimSlots - 1) / kSimSlots;
+            m = 0u;
+            for (int j = 0; j < G; ++j) {
+                double mx = -INFINITY;
+                for (int sb = 0; sb < nsb; ++sb)
+                    mx = fmax(mx, w.rho_bmax[(int64_t)(bh0 + j) * (kMaxCache / kSimSlots) + sb]);
+                if (mx < (double)a.tau) m |= 1u << j;
+            }
+        }
+        s_exmask = m;
     }
+    __syncthreads();
+    const uint32_t exmask = s_exmask;
     if (exmask == 0) return;
     const int64_t row0 = (int64_t)chunk * geo.scan_chunk_rows;
     if (row0 >= a.len) return;
     if (a.mode == MODE_SELECT && chunk == 0 && tid == 0) atomicAdd(&w.stats[STAT_SCANS], 1ull);
 
+    uint32_t *s_hist = (uint32_t *)lds;
     for (int i = tid; i < G * kHistBins; i += kScoreThreads) s_hist[i] = 0u;
     __syncthreads();
 
@@ -634,15 +387,18 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
                 float s0 = 0.0f;
 #pragma unroll
                 for (int s = 0; s < R::kNV; ++s) s0 = Dot<T>::f(kv[u][s], qv[j][s], s0);
-                acc[j] = quad_sum(s0);
+                acc[j] = s0;
             }
+            float sc_lo, sc_hi;
+            group_scores<G>(acc, p, sc_lo, sc_hi);
             if (row[u] < row_end) {
 #pragma unroll
                 for (int jj = 0; jj < (G + 3) / 4; ++jj) {
-                    const int j = jj * 4 + p;
-                    if (j < G && ((exmask >> j) & 1u)) {
-                        const float sc = pick<G>(acc, j) * a.inv_sqrt_d;
-                        w.scores[(int64_t)(bh0 + j) * a.max_len + row[u]] = sc;
+                    const int j = jj * 4 + (G == 1 ? 0 : (G == 2 ? (p & 1) : p));
+                    const bool mine = G == 1 ? p == 0 : (G == 2 ? p < 2 : true);
+                    if (mine && ((exmask >> j) & 1u)) {
+                        const float sc = (jj == 0 ? sc_lo : sc_hi) * a.inv_sqrt_d;
+                        w.scores[(int64_t)(bh0 + j) * a.row_stride + row[u]] = sc;
                         atomicAdd(&s_hist[j * kHistBins + (ord_key(sc) >> kHistShift)], 1u);
                     }
                 }
@@ -659,74 +415,176 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
     }
 }
 
+// Range block s of head bh: path rule, Top-R, the head's candidates inside index
+// range s, and their scores.  Entries go to region (bh, s) in index order.
 template <typename T, int D>
-__device__ void cand_block(const StepArgs &a, const Ws &w, const Geometry &geo, int cb)
+__device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned char *lds)
 {
     using R = RowT<T, D>;
-    constexpr int kIters = kCandRows / kScanRowsPerIter;
+    constexpr int NT = kScoreThreads;
+    __shared__ double s_red64[NT / 64];
+    __shared__ uint32_t s_red32[NT / 64];
+    __shared__ int32_t s_ret[kMaxR];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
-    const int bh = cb / geo.cand_blocks_per_head, cc = cb % geo.cand_blocks_per_head;
-    if (w.path[bh] != PATH_REUSE) return;
-    const int n = w.n_cand[bh];
-    if (cc * kCandRows >= n) return;
-    const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
+    const int bh = cb / kCandRanges, s = cb % kCandRanges;
+    const int M = a.M;
+    const int n_valid = (int)(a.n_ins < (int64_t)M ? a.n_ins : (int64_t)M);
+    double *s_rho = (double *)lds;
 
-    uint4 qv[R::kNV];
-    const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)bh * a.q_head_stride);
-#pragma unroll
-    for (int s = 0; s < R::kNV; ++s) qv[s] = qr[s * 4 + p];
-    const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
-    const int32_t *cl = w.cand + (int64_t)bh * a.cand_cap;
-    uint64_t *ce = w.cand_ent + (int64_t)bh * a.cand_cap;
+    // rho of every valid slot (written by k_sim), rho_max and the path (Eq. 13).
+    double mx = -INFINITY;
+    for (int i = tid; i < n_valid; i += NT) {
+        const double r = w.rho[(int64_t)bh * M + i];
+        s_rho[i] = r;
+        mx = fmax(mx, r);
+    }
+    mx = block_reduce<NT>(mx, s_red64, [](double x, double y) { return fmax(x, y); });
+    const int8_t path = mx < (double)a.tau ? PATH_FALLBACK : PATH_REUSE;
+    const int nret = path == PATH_REUSE ? (a.R < n_valid ? a.R : n_valid) : 0;
+    if (s == 0 && tid == 0) {
+        w.path[bh] = path;
+        if (a.dbg_path) a.dbg_path[bh] = path;
+        if (a.dbg_rho) a.dbg_rho[bh] = mx;
+        atomicAdd(&w.stats[path == PATH_REUSE ? STAT_REUSE : STAT_FALLBACK], 1ull);
+    }
+    if (path != PATH_REUSE) {
+        if (s == 0 && a.dbg_ret)
+            for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = -1;
+        return;
+    }
 
-    uint4 kv[kIters][R::kNV];
-    int ci[kIters], cidx[kIters];
-#pragma unroll
-    for (int u = 0; u < kIters; ++u) {
-        ci[u] = cc * kCandRows + u * kScanRowsPerIter + wave * 16 + rl;
-        cidx[u] = ci[u] < n ? cl[ci[u]] : 0;
-        if (ci[u] < n) {
-            const uint4 *rp = (const uint4 *)(kbase + (int64_t)cidx[u] * D);
-#pragma unroll
-            for (int s = 0; s < R::kNV; ++s) kv[u][s] = rp[s * 4 + p];
-        } else {
-#pragma unroll
-            for (int s = 0; s < R::kNV; ++s) kv[u][s] = make_uint4(0u, 0u, 0u, 0u);
+    // Eq. 7: slot i is the rank-th retrieved entry, rank = number of slots that are
+    // more similar, or equally similar and newer (age (n_ins-1-slot) mod C).
+    const int age0 = (int)(((a.n_ins - 1) % M + M) % M);
+    for (int i = tid; i < n_valid; i += NT) {
+        const double ri = s_rho[i];
+        const int ai = (age0 - i + M) % M;
+        int rank = 0;
+        for (int j = 0; j < n_valid && rank < nret; ++j) {
+            const double rj = s_rho[j];
+            const int aj = (age0 - j + M) % M;
+            rank += (rj > ri || (rj == ri && aj < ai)) ? 1 : 0;
         }
+        if (rank < nret) s_ret[rank] = i;
     }
+    __syncthreads();
+    if (s == 0 && a.dbg_ret)
+        for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = i < nret ? s_ret[i] : -1;
+
+    // Eq. 8-9 restricted to this block's index range [lo, hi).
+    const int64_t len = a.len;
+    const int64_t span = (len + kCandRanges - 1) / kCandRanges;
+    const int64_t lo = (int64_t)s * span;
+    const int64_t hi = lo + span < len ? lo + span : len;
+    const int64_t w0 = len - a.W > 0 ? len - a.W : 0;
+    uint32_t *bitmap = (uint32_t *)lds;                    // reuses the rho space
+    int32_t *list = (int32_t *)(lds + kSegWords * 4);
+    uint64_t *ents = w.cand_ent + ((int64_t)bh * kCandRanges + s) * a.cand_cap;
+    const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
+    const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
+    uint4 qv[R::kNV];
+    {
+        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)bh * a.q_head_stride);
 #pragma unroll
-    for (int u = 0; u < kIters; ++u) {
-        float s0 = 0.0f;
-#pragma unroll
-        for (int s = 0; s < R::kNV; ++s) s0 = Dot<T>::f(kv[u][s], qv[s], s0);
-        s0 = quad_sum(s0);
-        if (p == 0 && ci[u] < n) ce[ci[u]] = rank_of(s0 * a.inv_sqrt_d, (uint32_t)cidx[u]);
+        for (int v = 0; v < R::kNV; ++v) qv[v] = qr[v * 4 + p];
     }
+    __syncthreads();   // s_rho is dead from here on
+
+    int total = 0;
+    for (int64_t seg = lo; seg < hi; seg += (int64_t)kSegWords * 32) {
+        const int64_t seg_hi = seg + (int64_t)kSegWords * 32 < hi ? seg + (int64_t)kSegWords * 32 : hi;
+        const int nwords = (int)((seg_hi - seg + 31) >> 5);
+        for (int i = tid; i < nwords; i += NT) bitmap[i] = 0u;
+        __syncthreads();
+        for (int r = 0; r < nret; ++r) {
+            const int64_t e = (int64_t)bh * M + s_ret[r];
+            const int32_t *sp = w.supp + e * a.K;
+            const int c = w.cnt[e];
+            for (int t = tid; t < c; t += NT) {
+                const int64_t x = sp[t];
+                if (x >= seg && x < seg_hi) atomicOr(&bitmap[(x - seg) >> 5], 1u << ((x - seg) & 31));
+            }
+        }
+        for (int64_t x = (w0 > seg ? w0 : seg) + tid; x < seg_hi; x += NT)
+            atomicOr(&bitmap[(x - seg) >> 5], 1u << ((x - seg) & 31));
+        __syncthreads();
+        const int wpt = (nwords + NT - 1) / NT;
+        const int wb = tid * wpt < nwords ? tid * wpt : nwords;
+        const int we = wb + wpt < nwords ? wb + wpt : nwords;
+        uint32_t mine = 0;
+        for (int i = wb; i < we; ++i) mine += __popc(bitmap[i]);
+        uint32_t seg_total;
+        const uint32_t first = block_excl_scan<NT>(mine, s_red32, &seg_total);
+        for (uint32_t rb = 0; rb < seg_total; rb += kCandList) {
+            // emit this round's candidates (ascending) into the LDS list
+            uint32_t pos = first;
+            for (int i = wb; i < we && pos < rb + kCandList; ++i) {
+                uint32_t bits = bitmap[i];
+                while (bits) {
+                    const int bit = __ffs(bits) - 1;
+                    bits &= bits - 1u;
+                    if (pos >= rb && pos < rb + kCandList)
+                        list[pos - rb] = (int32_t)(seg + (int64_t)i * 32 + bit);
+                    ++pos;
+                }
+            }
+            __syncthreads();
+            const int nr = (int)(seg_total - rb < (uint32_t)kCandList ? seg_total - rb : kCandList);
+            // Eq. 10 on this round: 4 lanes per key row, two rows per lane in flight.
+            for (int base = 0; base < nr; base += 2 * kScanRowsPerIter) {
+                uint4 kv[2][R::kNV];
+                int ci[2], cidx[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    ci[u] = base + u * kScanRowsPerIter + wave * 16 + rl;
+                    cidx[u] = ci[u] < nr ? list[ci[u]] : 0;
+                    const uint4 *rp = (const uint4 *)(kbase + (int64_t)cidx[u] * D);
+#pragma unroll
+                    for (int v = 0; v < R::kNV; ++v)
+                        kv[u][v] = ci[u] < nr ? rp[v * 4 + p] : make_uint4(0u, 0u, 0u, 0u);
+                }
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    float s0 = 0.0f;
+#pragma unroll
+                    for (int v = 0; v < R::kNV; ++v) s0 = Dot<T>::f(kv[u][v], qv[v], s0);
+                    s0 = quad_sum(s0);
+                    if (p == 0 && ci[u] < nr)
+                        ents[total + rb + ci[u]] = rank_of(s0 * a.inv_sqrt_d, (uint32_t)cidx[u]);
+                }
+            }
+            __syncthreads();
+        }
+        total += (int)seg_total;
+    }
+    if (tid == 0) w.cand_cnt[(int64_t)bh * kCandRanges + s] = (uint32_t)total;
 }
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(kScoreThreads) void k_score(StepArgs a, Ws w, Geometry geo)
 {
-    __shared__ uint32_t s_hist[G * kHistBins];
+    __shared__ __attribute__((aligned(16))) unsigned char lds[ScoreLds<G>::kBytes];
     if ((int)blockIdx.x < geo.scan_blocks)
-        scan_block<T, D, G>(a, w, geo, s_hist);
+        scan_block<T, D, G>(a, w, geo, lds);
     else
-        cand_block<T, D>(a, w, geo, (int)blockIdx.x - geo.scan_blocks);
+        range_block<T, D>(a, w, (int)blockIdx.x - geo.scan_blocks, lds);
 }
 
 // ---------------------------------------------------------------------------
-// k_filter: the surviving scores of every exact head
+// k_filter: survivors of every exact head, compacted in index order per block
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geometry geo)
 {
     constexpr int NT = kScoreThreads;
+    constexpr int EPT = kFilterRows / NT;   // 8 consecutive scores per thread
     static_assert(NT * 4 == kHistBins, "4 histogram bins per thread");
+    static_assert(EPT == 8, "two float4 per thread");
     __shared__ uint32_t s_red[NT / 64];
     __shared__ uint32_t s_bstar;
     const int tid = threadIdx.x;
     const int bh = blockIdx.x / geo.filter_blocks_per_head;
-    const int fc = blockIdx.x % geo.filter_blocks_per_head;
+    const int f = blockIdx.x % geo.filter_blocks_per_head;
     if (a.mode == MODE_SELECT && w.path[bh] == PATH_REUSE) return;
 
     // The bin b* that holds the kn-th largest score: the largest b with
@@ -737,8 +595,8 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
         uint32_t c[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) c[j] = hist[kHistBins - 1 - 4 * tid - j];
-        uint32_t tot = c[0] + c[1] + c[2] + c[3], all;
-        uint32_t above = block_excl_scan<NT>(tot, s_red, &all);
+        uint32_t all;
+        uint32_t above = block_excl_scan<NT>(c[0] + c[1] + c[2] + c[3], s_red, &all);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             if (above < kn && above + c[j] >= kn) s_bstar = (uint32_t)(kHistBins - 1 - 4 * tid - j);
@@ -747,73 +605,292 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
         __syncthreads();
     }
     const uint32_t kmin = s_bstar << kHistShift;
-    const float *sc = w.scores + (int64_t)bh * a.max_len;
-    uint64_t *sv = w.surv + (int64_t)bh * a.max_len;
-    const int64_t i0 = (int64_t)fc * kFilterRows;
-    float s[kFilterRows / NT];
+    const int64_t i0 = (int64_t)f * kFilterRows + (int64_t)tid * EPT;
+    const float4 *src = (const float4 *)(w.scores + (int64_t)bh * a.row_stride + i0);
+    const float4 v0 = src[0], v1 = src[1];
+    const float sv[EPT] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    uint32_t keep = 0, n = 0;
 #pragma unroll
-    for (int it = 0; it < kFilterRows / NT; ++it) {
-        const int64_t i = i0 + (int64_t)it * NT + tid;
-        s[it] = i < a.len ? sc[i] : 0.0f;
+    for (int e = 0; e < EPT; ++e) {
+        const bool k = i0 + e < a.len && ord_key(sv[e]) >= kmin;
+        keep |= (uint32_t)k << e;
+        n += k ? 1u : 0u;
     }
+    uint32_t total;
+    uint32_t pos = block_excl_scan<NT>(n, s_red, &total);
+    uint64_t *dst = w.surv + (int64_t)bh * a.row_stride + (int64_t)f * kFilterRows;
 #pragma unroll
-    for (int it = 0; it < kFilterRows / NT; ++it) {
-        const int64_t i = i0 + (int64_t)it * NT + tid;
-        const bool keep = i < a.len && ord_key(s[it]) >= kmin;
-        const uint64_t m = __ballot(keep);
-        if (m) {
-            const int lane = tid & 63;
-            const int leader = __ffsll((unsigned long long)m) - 1;
-            uint32_t base = 0;
-            if (lane == leader) base = atomicAdd(&w.surv_count[bh], (uint32_t)__popcll(m));
-            base = __shfl(base, leader);
-            const uint32_t off = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                     __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-            if (keep) sv[base + off] = rank_of(s[it], (uint32_t)i);
-        }
-    }
+    for (int e = 0; e < EPT; ++e)
+        if ((keep >> e) & 1u) dst[pos++] = rank_of(sv[e], (uint32_t)(i0 + e));
+    if (tid == 0) w.surv_cnt[(int64_t)bh * a.n_regions + f] = total;
 }
 
 // ---------------------------------------------------------------------------
-// k_final: one block per query head
+// k_final
 // ---------------------------------------------------------------------------
 
+template <int D, int NT>
+struct FinalSmem {
+    uint64_t ent[kEntCache];        // the head's entries in index order, when they fit
+    uint64_t sel[kMaxK];            // selected (index << 32 | score key), index order
+    float wgt[kMaxK];
+    uint32_t pref[kMaxRegions + 1]; // region prefix counts
+    uint32_t hist[kHistBins];
+    float part[NT / 64][D / kFinalSlices];
+    float qbar[D];
+    double red64[NT / 64];
+    float red32[NT / 64];
+    uint32_t redu[NT / 64];
+    uint32_t found_digit, found_above, found_cnt;
+};
+
+// Entries of one head, spread over regions of a fixed stride, read in order.
+struct Regions {
+    const uint64_t *base;
+    int64_t stride;
+    int n;
+    const uint64_t *staged;   // LDS copy or nullptr
+    const uint32_t *pref;
+    int nreg;
+    __device__ uint64_t get(int j) const
+    {
+        if (staged) return staged[j];
+        int lo = 0, hi = nreg - 1;   // last region r with pref[r] <= j
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if ((int)pref[mid] <= j) lo = mid; else hi = mid - 1;
+        }
+        return base[(int64_t)lo * stride + (j - (int)pref[lo])];
+    }
+};
+
+// Radix select over distinct 64-bit ranks with 11-bit digits, most significant
+// first.  On return the top min(K, n) entries are exactly those with
+// (rank & mask) >= prefix (mask == 0 selects everything).
+template <int D, int NT>
+__device__ void radix_threshold(const Regions &rg, int K, FinalSmem<D, NT> &sm, uint64_t &prefix,
+                                uint64_t &mask)
+{
+    const int tid = threadIdx.x;
+    prefix = 0;
+    mask = 0;
+    if (rg.n <= K) return;
+    uint32_t k_rem = (uint32_t)K;
+    for (int shift = 53; ; shift -= 11) {
+        const int sh = shift > 0 ? shift : 0;
+        const int width = shift > 0 ? 11 : 11 + shift;
+        const uint32_t nb = 1u << width;
+        for (uint32_t i = tid; i < nb; i += NT) sm.hist[i] = 0u;
+        __syncthreads();
+        for (int j = tid; j < rg.n; j += NT) {
+            const uint64_t e = rg.get(j);
+            if ((e & mask) == prefix) atomicAdd(&sm.hist[(uint32_t)(e >> sh) & (nb - 1u)], 1u);
+        }
+        __syncthreads();
+        // thread t covers digits nb-1-4t .. nb-4-4t (descending)
+        uint32_t c[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int dgt = (int)nb - 1 - 4 * tid - j;
+            c[j] = dgt >= 0 ? sm.hist[dgt] : 0u;
+        }
+        uint32_t all;
+        uint32_t above = block_excl_scan<NT>(c[0] + c[1] + c[2] + c[3], sm.redu, &all);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (above < k_rem && above + c[j] >= k_rem) {
+                sm.found_digit = nb - 1u - 4u * tid - j;
+                sm.found_above = above;
+                sm.found_cnt = c[j];
+            }
+            above += c[j];
+        }
+        __syncthreads();
+        k_rem -= sm.found_above;
+        prefix |= (uint64_t)sm.found_digit << sh;
+        mask |= (uint64_t)(nb - 1u) << sh;
+        const bool done = sm.found_cnt == k_rem || sh == 0;
+        __syncthreads();
+        if (done) break;
+    }
+}
+
 template <typename T, int D>
-__global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w, Geometry geo)
+__global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
 {
     constexpr int NT = kFinalThreads;
+    constexpr int NW = NT / 64;
+    constexpr int DS = D / kFinalSlices;                 // elements per slice
+    constexpr int SB = DS * (int)sizeof(T);              // bytes per slice row
+    constexpr int LPR = SB / 16;                         // lanes per slice row
+    constexpr int RPW = 64 / LPR;                        // rows per wave instruction
+    constexpr int EPV = 16 / (int)sizeof(T);
+    static_assert(SB % 16 == 0 && LPR >= 1 && LPR <= 64, "slice geometry");
     __shared__ FinalSmem<D, NT> sm;
-    const int tid = threadIdx.x;
-    const int bh = blockIdx.x;
-    (void)geo;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int bh = blockIdx.x / kFinalSlices, slice = blockIdx.x % kFinalSlices;
+    const bool writes_out = a.out != nullptr && a.mode != MODE_PREFILL;
+    if (slice != 0 && !writes_out) return;
 
-    if (a.mode == MODE_REFRESH || a.mode == MODE_COLD) {
+    if (slice == 0 && (a.mode == MODE_REFRESH || a.mode == MODE_COLD)) {
         const int8_t code = a.mode == MODE_REFRESH ? PATH_REFRESH : PATH_COLD;
         if (tid == 0) {
             if (a.dbg_path) a.dbg_path[bh] = code;
             if (a.dbg_rho) a.dbg_rho[bh] = __builtin_nan("");
-            if (a.dbg_ncand) a.dbg_ncand[bh] = 0;
         }
         if (a.dbg_ret)
             for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = -1;
-        if (a.dbg_cand)
-            for (int i = tid; i < a.cand_cap; i += NT) a.dbg_cand[(int64_t)bh * a.cand_cap + i] = -1;
     }
     const bool reuse = a.mode == MODE_SELECT && w.path[bh] == PATH_REUSE;
+
+    // Region layout of this head's entries.
+    Regions rg;
+    const uint32_t *cnts;
     if (reuse) {
-        finalize_head<T, D, NT>(a, w, bh, w.cand_ent + (int64_t)bh * a.cand_cap, w.n_cand[bh], sm);
+        rg.base = w.cand_ent + (int64_t)bh * kCandRanges * a.cand_cap;
+        rg.stride = a.cand_cap;
+        rg.nreg = kCandRanges;
+        cnts = w.cand_cnt + (int64_t)bh * kCandRanges;
     } else {
-        const int n = (int)w.surv_count[bh];
-        finalize_head<T, D, NT>(a, w, bh, w.surv + (int64_t)bh * a.max_len, n, sm);
-        // Leave the exact-path workspace zeroed for the next launch.
-        for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)bh * kHistBins + i] = 0u;
-        if (tid == 0) w.surv_count[bh] = 0u;
+        rg.base = w.surv + (int64_t)bh * a.row_stride;
+        rg.stride = kFilterRows;
+        rg.nreg = (int)((a.len + kFilterRows - 1) / kFilterRows);
+        cnts = w.surv_cnt + (int64_t)bh * a.n_regions;
     }
+    {
+        // prefix over region counts: thread t owns regions [t*rpt, ...)
+        const int rpt = (rg.nreg + NT - 1) / NT;
+        const int r0 = tid * rpt < rg.nreg ? tid * rpt : rg.nreg;
+        const int r1 = r0 + rpt < rg.nreg ? r0 + rpt : rg.nreg;
+        uint32_t mine = 0;
+        for (int r = r0; r < r1; ++r) mine += cnts[r];
+        uint32_t total;
+        uint32_t run = block_excl_scan<NT>(mine, sm.redu, &total);
+        for (int r = r0; r < r1; ++r) {
+            sm.pref[r] = run;
+            run += cnts[r];
+        }
+        if (tid == 0) sm.pref[rg.nreg] = total;
+        __syncthreads();
+        rg.n = (int)total;
+    }
+    rg.pref = sm.pref;
+    rg.staged = nullptr;
+    if (rg.n <= kEntCache) {
+        for (int j = tid; j < rg.n; j += NT) sm.ent[j] = rg.get(j);
+        __syncthreads();
+        rg.staged = sm.ent;
+    }
+
+    // Top-K (Eq. 1 / Eq. 11), then the selected entries in index order.
+    uint64_t prefix, mask;
+    radix_threshold<D, NT>(rg, a.K, sm, prefix, mask);
+    const int kn = rg.n < a.K ? rg.n : a.K;
+    {
+        const int ept = (rg.n + NT - 1) / NT;
+        const int j0 = tid * ept < rg.n ? tid * ept : rg.n;
+        const int j1 = j0 + ept < rg.n ? j0 + ept : rg.n;
+        uint32_t mine = 0;
+        for (int j = j0; j < j1; ++j) mine += ((rg.get(j) & mask) >= prefix) ? 1u : 0u;
+        uint32_t total;
+        uint32_t pos = block_excl_scan<NT>(mine, sm.redu, &total);
+        for (int j = j0; j < j1; ++j) {
+            const uint64_t e = rg.get(j);
+            if ((e & mask) >= prefix && pos < (uint32_t)kMaxK)
+                sm.sel[pos++] = ((uint64_t)rank_index(e) << 32) | rank_key(e);
+        }
+        __syncthreads();
+    }
+
+    if (writes_out) {
+        // Eq. 12 on this block's slice of the head dimension.
+        float mx = -INFINITY;
+        for (int t = tid; t < kn; t += NT) mx = fmaxf(mx, key_score((uint32_t)sm.sel[t]));
+        mx = block_reduce<NT>(mx, sm.red32, [](float x, float y) { return fmaxf(x, y); });
+        float lsum = 0.0f;
+        for (int t = tid; t < kn; t += NT) {
+            const float wt = expf(key_score((uint32_t)sm.sel[t]) - mx);
+            sm.wgt[t] = wt;
+            lsum += wt;
+        }
+        lsum = block_reduce<NT>(lsum, sm.red32, [](float x, float y) { return x + y; });
+        const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
+        const T *vbase = (const T *)a.v + ((int64_t)b * a.Hkv + g) * a.max_len * D + slice * DS;
+        const int sub = lane / LPR, vl = lane % LPR;
+        float acc[EPV];
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) acc[e] = 0.0f;
+#pragma unroll 4
+        for (int t = wave * RPW + sub; t < kn; t += NW * RPW) {
+            const uint32_t idx = (uint32_t)(sm.sel[t] >> 32);
+            const uint4 raw = ((const uint4 *)(vbase + (int64_t)idx * D))[vl];
+            Dot<T>::axpy(raw, sm.wgt[t], acc);
+        }
+#pragma unroll
+        for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) acc[e] += __shfl_xor(acc[e], o);
+        if (sub == 0)
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) sm.part[wave][vl * EPV + e] = acc[e];
+        __syncthreads();
+        if (tid < DS) {
+            float o = 0.0f;
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) o += sm.part[ww][tid];
+            a.out[(int64_t)bh * D + slice * DS + tid] = kn > 0 ? o / lsum : 0.0f;
+        }
+    }
+    if (slice != 0) return;
+
+    if (writes_out && a.sel != nullptr)
+        for (int t = tid; t < a.K; t += NT)
+            a.sel[(int64_t)bh * a.K + t] = t < kn ? (int32_t)(sm.sel[t] >> 32) : -1;
+    if (a.do_insert) {
+        // Sec. 3.4: insert (q_bar, support) after either path.
+        const int64_t e = (int64_t)bh * a.M + a.insert_slot;
+        if (a.mode == MODE_SELECT) {
+            for (int t = tid; t < D; t += NT) w.qbar[e * D + t] = w.qbar_cur[(int64_t)bh * D + t];
+        } else {
+            const T *q = (const T *)a.q + (int64_t)bh * a.q_head_stride;
+            block_qbar<T, D, NT>(q, sm.qbar, sm.red64);
+            for (int t = tid; t < D; t += NT) w.qbar[e * D + t] = sm.qbar[t];
+        }
+        for (int t = tid; t < a.K; t += NT)
+            w.supp[e * a.K + t] = t < kn ? (int32_t)(sm.sel[t] >> 32) : -1;
+        if (tid == 0) w.cnt[e] = kn;
+    }
+    if (reuse) {
+        if (tid == 0) {
+            atomicAdd(&w.stats[STAT_CAND_SUM], (unsigned long long)rg.n);
+            atomicMax(&w.stats[STAT_CAND_MAX], (unsigned long long)rg.n);
+        }
+    } else {
+        // leave the histogram zeroed for the next launch
+        for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)bh * kHistBins + i] = 0u;
+    }
+    if (a.dbg_ncand && tid == 0) a.dbg_ncand[bh] = reuse ? rg.n : 0;
+    if (a.dbg_cand)
+        for (int j = tid; j < a.cand_cap; j += NT)
+            a.dbg_cand[(int64_t)bh * a.cand_cap + j] = (reuse && j < rg.n) ? (int32_t)rank_index(rg.get(j)) : -1;
 }
 
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
+
+// Launch on stream s; with a start/stop event pair the events are attached to the
+// dispatch itself, so they time exactly this kernel.
+template <typename F, typename... Args>
+static hipError_t launch(F kernel, dim3 grid, dim3 block, hipStream_t s, const Timing &tm,
+                         Args... args)
+{
+    if (tm.start != nullptr)
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, s, tm.start, tm.stop, 0, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+    return hipGetLastError();
+}
 
 bool shape_supported(int dtype, int d, int g)
 {
@@ -822,83 +899,68 @@ bool shape_supported(int dtype, int d, int g)
 }
 
 template <typename T, int D>
-static hipError_t select_impl(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
+static hipError_t sim_impl(const StepArgs &a, const Ws &w, hipStream_t s, const Timing &tm)
 {
-    hipLaunchKernelGGL((k_select<T, D>), dim3((unsigned)(a.B * a.Hq)), dim3(kSelectThreads), 0, s,
-                       a, w, geo);
-    return hipGetLastError();
+    const int nsb = (a.M + kSimSlots - 1) / kSimSlots;
+    return launch(k_sim<T, D>, dim3((unsigned)(a.B * a.Hq * nsb)), dim3(kSimThreads), s, tm, a, w);
 }
 
 template <typename T, int D, int G>
-static hipError_t score_impl(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
+static hipError_t score_impl(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s,
+                             const Timing &tm)
 {
-    const int blocks = geo.scan_blocks + a.B * a.Hq * geo.cand_blocks_per_head;
-    if (blocks == 0) return hipSuccess;
-    hipLaunchKernelGGL((k_score<T, D, G>), dim3((unsigned)blocks), dim3(kScoreThreads), 0, s, a, w, geo);
-    return hipGetLastError();
-}
-
-static hipError_t filter_impl(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
-{
-    dim3 grid((unsigned)(a.B * a.Hq * geo.filter_blocks_per_head));
-    hipLaunchKernelGGL(k_filter, grid, dim3(kScoreThreads), 0, s, a, w, geo);
-    return hipGetLastError();
+    const int blocks = geo.scan_blocks + geo.cand_blocks;
+    return launch(k_score<T, D, G>, dim3((unsigned)blocks), dim3(kScoreThreads), s, tm, a, w, geo);
 }
 
 template <typename T, int D>
-static hipError_t final_impl(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
+static hipError_t final_impl(const StepArgs &a, const Ws &w, hipStream_t s, const Timing &tm)
 {
-    hipLaunchKernelGGL((k_final<T, D>), dim3((unsigned)(a.B * a.Hq)), dim3(kFinalThreads), 0, s,
-                       a, w, geo);
-    return hipGetLastError();
+    return launch(k_final<T, D>, dim3((unsigned)(a.B * a.Hq * kFinalSlices)), dim3(kFinalThreads),
+                  s, tm, a, w);
 }
 
-template <typename T>
-static hipError_t select_d(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
-{
-    return a.D == 64 ? select_impl<T, 64>(a, w, geo, s) : select_impl<T, 128>(a, w, geo, s);
-}
-template <typename T>
-static hipError_t final_d(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
-{
-    return a.D == 64 ? final_impl<T, 64>(a, w, geo, s) : final_impl<T, 128>(a, w, geo, s);
-}
 template <typename T, int D>
-static hipError_t score_g(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
+static hipError_t score_g(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s,
+                          const Timing &tm)
 {
     switch (a.G) {
-    case 1: return score_impl<T, D, 1>(a, w, geo, s);
-    case 2: return score_impl<T, D, 2>(a, w, geo, s);
-    case 4: return score_impl<T, D, 4>(a, w, geo, s);
-    default: return score_impl<T, D, 8>(a, w, geo, s);
+    case 1: return score_impl<T, D, 1>(a, w, geo, s, tm);
+    case 2: return score_impl<T, D, 2>(a, w, geo, s, tm);
+    case 4: return score_impl<T, D, 4>(a, w, geo, s, tm);
+    default: return score_impl<T, D, 8>(a, w, geo, s, tm);
     }
 }
-template <typename T>
-static hipError_t score_d(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s)
-{
-    return a.D == 64 ? score_g<T, 64>(a, w, geo, s) : score_g<T, 128>(a, w, geo, s);
-}
 
-hipError_t launch_select(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                         hipStream_t s)
+hipError_t launch_sim(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
+                      hipStream_t s, const Timing &tm)
 {
-    return dtype == 1 ? select_d<uint16_t>(a, w, geo, s) : select_d<float>(a, w, geo, s);
+    (void)geo;
+    if (dtype == 1)
+        return a.D == 64 ? sim_impl<uint16_t, 64>(a, w, s, tm) : sim_impl<uint16_t, 128>(a, w, s, tm);
+    return a.D == 64 ? sim_impl<float, 64>(a, w, s, tm) : sim_impl<float, 128>(a, w, s, tm);
 }
 hipError_t launch_score(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                        hipStream_t s)
+                        hipStream_t s, const Timing &tm)
 {
-    return dtype == 1 ? score_d<uint16_t>(a, w, geo, s) : score_d<float>(a, w, geo, s);
+    if (dtype == 1)
+        return a.D == 64 ? score_g<uint16_t, 64>(a, w, geo, s, tm) : score_g<uint16_t, 128>(a, w, geo, s, tm);
+    return a.D == 64 ? score_g<float, 64>(a, w, geo, s, tm) : score_g<float, 128>(a, w, geo, s, tm);
 }
 hipError_t launch_filter(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                         hipStream_t s)
+                         hipStream_t s, const Timing &tm)
 {
     (void)dtype;
-    return filter_impl(a, w, geo, s);
+    return launch(k_filter, dim3((unsigned)(a.B * a.Hq * geo.filter_blocks_per_head)),
+                  dim3(kScoreThreads), s, tm, a, w, geo);
 }
 hipError_t launch_final(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                        hipStream_t s)
+                        hipStream_t s, const Timing &tm)
 {
-    return dtype == 1 ? final_d<uint16_t>(a, w, geo, s) : final_d<float>(a, w, geo, s);
+    (void)geo;
+    if (dtype == 1)
+        return a.D == 64 ? final_impl<uint16_t, 64>(a, w, s, tm) : final_impl<uint16_t, 128>(a, w, s, tm);
+    return a.D == 64 ? final_impl<float, 64>(a, w, s, tm) : final_impl<float, 128>(a, w, s, tm);
 }
 
 }  // namespace retopk
