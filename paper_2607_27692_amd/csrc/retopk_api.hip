@@ -63,6 +63,7 @@ retopk_status validate_config(const retopk_config *c)
         return RETOPK_ERR_ARG;
     if (!std::isfinite(c->tau)) return RETOPK_ERR_ARG;
     if (c->k > kMaxK || c->cache_cap > kMaxCache || c->r > kMaxR) return RETOPK_ERR_UNSUPPORTED;
+    if ((int64_t)c->batch * c->n_q_heads > kMaxHeads) return RETOPK_ERR_UNSUPPORTED;
     if ((int64_t)c->r * c->k + c->window >= ((int64_t)1 << 30)) return RETOPK_ERR_UNSUPPORTED;
     if (!shape_supported(c->dtype, c->head_dim, c->n_q_heads / c->n_kv_heads))
         return RETOPK_ERR_UNSUPPORTED;
@@ -111,23 +112,16 @@ StepArgs base_args(const retopk_handle_s *h)
     return a;
 }
 
-// Rows per scan block: about 256 blocks per (b, KV head), so that one KV group's
-// scan alone spreads over every CU; 256..4096 rows, a multiple of the 256 rows
-// one block pass covers.
-int scan_chunk_rows(int64_t len)
-{
-    int64_t want = ceil_div(len, 256);
-    int64_t rows = 256;
-    while (rows < want && rows < 4096) rows <<= 1;
-    return (int)rows;
-}
-
 Geometry make_geometry(const retopk_handle_s *h, int64_t len, int mode)
 {
     const retopk_config &c = h->cfg;
     Geometry g{};
-    g.scan_chunk_rows = scan_chunk_rows(len);
-    g.scan_blocks = (int)((int64_t)c.batch * c.n_kv_heads * ceil_div(len, g.scan_chunk_rows));
+    // Enough scan blocks to cover the whole chip when every group is scanned;
+    // fewer in MODE_SELECT, where the range blocks share the chip.
+    const int64_t rows = (int64_t)c.batch * c.n_kv_heads * len;
+    const int64_t want = ceil_div(rows, 2 * kScanRowsPerIter);
+    const int cap = mode == MODE_SELECT ? kScanBlocksSelect : kScanBlocksExact;
+    g.scan_blocks = (int)(want < cap ? want : cap);
     g.cand_blocks = mode == MODE_SELECT ? (int)(heads_of(c) * kCandRanges) : 0;
     g.filter_blocks_per_head = (int)ceil_div(len, kFilterRows);
     return g;
@@ -235,6 +229,9 @@ retopk_status retopk_create(const retopk_config *cfg, retopk_handle *out)
         (st = alloc(h, &w.cnt, (size_t)(BH * C))) != RETOPK_OK ||
         (st = alloc(h, &w.rho, (size_t)(BH * C))) != RETOPK_OK ||
         (st = alloc(h, &w.rho_bmax, (size_t)(BH * NSB))) != RETOPK_OK ||
+        (st = alloc(h, &w.topr, (size_t)(BH * NSB * kMaxR))) != RETOPK_OK ||
+        (st = alloc(h, &w.topr_rho, (size_t)(BH * NSB * kMaxR))) != RETOPK_OK ||
+        (st = alloc(h, &w.topr_cnt, (size_t)(BH * NSB * kMaxR))) != RETOPK_OK ||
         (st = alloc(h, &w.qbar_cur, (size_t)(BH * D))) != RETOPK_OK ||
         (st = alloc(h, &w.path, (size_t)BH)) != RETOPK_OK ||
         (st = alloc(h, &w.scores, (size_t)(BH * RS))) != RETOPK_OK ||

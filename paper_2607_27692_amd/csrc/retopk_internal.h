@@ -18,7 +18,7 @@ constexpr int kScoreThreads = 512;    // k_score and k_filter blocks
 constexpr int kFinalThreads = 512;    // k_final blocks
 constexpr int kFinalSlices = 4;       // k_final blocks per head (one d-slice of V each)
 constexpr int kScanRowsPerIter = 128; // 8 waves x 16 rows
-constexpr int kCandRanges = 16;       // index ranges (k_score blocks) per reuse head
+constexpr int kCandRanges = 8;        // index ranges (k_score blocks) per reuse head
 constexpr int kCandList = 2048;       // candidates gathered per round in one range block
 constexpr int kSegWords = 2048;       // union bitmap segment: 65536 indices
 constexpr int kFilterRows = 4096;     // scores filtered per k_filter block
@@ -27,6 +27,9 @@ constexpr int kMaxRegions = 4096;     // filter regions per head (max_len <= 16M
 constexpr int kMaxK = 2048;
 constexpr int kMaxR = 32;
 constexpr int kMaxCache = 4096;
+constexpr int kMaxHeads = 2048;       // B * Hq
+constexpr int kScanBlocksSelect = 256;  // k_score scan blocks in MODE_SELECT
+constexpr int kScanBlocksExact = 2048;  // k_score scan blocks when every head is exact
 constexpr int64_t kMaxLen = (int64_t)kMaxRegions * kFilterRows;
 
 // Step modes.  SELECT runs the per-head path rule on the device; the others take
@@ -57,6 +60,9 @@ struct Ws {
     // per-step workspaces
     double *rho;          // [BH, C] cosine similarities of this step
     double *rho_bmax;     // [BH, kMaxCache / kSimSlots] per-k_sim-block maxima of rho
+    int32_t *topr;        // [BH, kMaxCache / kSimSlots, kMaxR] per-k_sim-block Top-R slots
+    double *topr_rho;     // [BH, kMaxCache / kSimSlots, kMaxR] their similarities
+    int32_t *topr_cnt;    // [BH, kMaxCache / kSimSlots, kMaxR] their support sizes
     float *qbar_cur;      // [BH, d] q_bar of this step
     int8_t *path;         // [BH] path of this step
     float *scores;        // [BH, row_stride] full-history scores of exact heads
@@ -99,8 +105,7 @@ struct StepArgs {
 
 // Launch geometry chosen on the host.
 struct Geometry {
-    int scan_chunk_rows;
-    int scan_blocks;           // B * Hkv * chunks
+    int scan_blocks;           // scan blocks of k_score (they split the scanned rows)
     int cand_blocks;           // B * Hq * kCandRanges in MODE_SELECT, else 0
     int filter_blocks_per_head;
 };

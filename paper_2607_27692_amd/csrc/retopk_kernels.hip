@@ -261,12 +261,26 @@ __device__ void block_qbar(const T *q, float *s_qbar, double *red)
 // k_sim: rho for 64 cache slots per block (Eq. 6)
 // ---------------------------------------------------------------------------
 
+__device__ __forceinline__ bool better(double ra, int aa, double rb, int ab)
+{
+    return ra > rb || (ra == rb && aa < ab);
+}
+
+// Age of a cache slot: 0 for the most recent insertion, (n_ins - 1 - slot) mod C.
+__device__ __forceinline__ int slot_age(int age0, int slot, int M)
+{
+    const int a = age0 - slot;
+    return a < 0 ? a + M : a;
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
 {
     constexpr int NT = kSimThreads;
     __shared__ float s_qbar[D];
     __shared__ double s_red[NT / 64];
+    __shared__ double s_rho[kSimSlots];
+    __shared__ int s_age[kSimSlots];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3;
     const int M = a.M;
     const int nsb = (M + kSimSlots - 1) / kSimSlots;
@@ -277,13 +291,14 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
     if (sb == 0)
         for (int t = tid; t < D; t += NT) w.qbar_cur[(int64_t)bh * D + t] = s_qbar[t];
 
-    // 16 slots per wave, 4 lanes per cached row of D floats.
-    const int slot = sb * kSimSlots + wave * 16 + (lane >> 2);
+    // Eq. 6: 16 slots per wave, 4 lanes per cached row of D floats.
+    const int local = wave * 16 + (lane >> 2);
+    const int slot = sb * kSimSlots + local;
     const float4 *crow = (const float4 *)(w.qbar + ((int64_t)bh * M + (slot < n_valid ? slot : 0)) * D);
     float4 c[D / 16];
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s)
-        c[s] = slot < n_valid ? crow[s * 4 + p] : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s = 0; s < D / 16; ++s) c[s] = crow[s * 4 + p];   // clamped row: always in bounds
+    const int scnt = w.cnt[(int64_t)bh * M + (slot < n_valid ? slot : 0)];
     double acc = 0.0;
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
@@ -294,66 +309,69 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
         acc += (double)c[s].w * (double)qq[3];
     }
     acc = quad_sum(acc);
-    if (slot < n_valid && p == 0) w.rho[(int64_t)bh * M + slot] = acc;
-    const double bmax = block_reduce<NT>(slot < n_valid ? acc : -INFINITY, s_red,
-                                         [](double x, double y) { return fmax(x, y); });
-    if (tid == 0) w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = bmax;
+    const int age0 = (int)((a.n_ins - 1) % M);
+    if (p == 0) {
+        s_rho[local] = slot < n_valid ? acc : -INFINITY;
+        s_age[local] = slot < n_valid ? slot_age(age0, slot, M) : 0x7FFFFFFF;
+        if (slot < n_valid) w.rho[(int64_t)bh * M + slot] = acc;
+    }
+    __syncthreads();
+
+    // This block's Top-R slots (Eq. 7) by rank counting: the 4 lanes of a quad
+    // compare slot `local` against 16 slots each; rank = number of slots that are
+    // more similar, or equally similar and newer.  The global Top-R is contained
+    // in the union of the blocks' lists.
+    {
+        const double ri = s_rho[local];
+        const int ai = s_age[local];
+        int cnt = 0;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int o = p * 16 + u;
+            cnt += better(s_rho[o], s_age[o], ri, ai) ? 1 : 0;
+        }
+        cnt += __builtin_amdgcn_mov_dpp(cnt, kQuadXor1, 0xF, 0xF, true);
+        cnt += __builtin_amdgcn_mov_dpp(cnt, kQuadXor2, 0xF, 0xF, true);
+        const int64_t base = ((int64_t)bh * (kMaxCache / kSimSlots) + sb) * kMaxR;
+        if (p == 0 && slot < n_valid && cnt < a.R) {
+            w.topr[base + cnt] = slot;
+            w.topr_rho[base + cnt] = ri;
+            w.topr_cnt[base + cnt] = scnt;
+            if (cnt == 0) w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = ri;
+        }
+        if (tid == 0 && sb * kSimSlots >= n_valid)
+            w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = -INFINITY;
+    }
 }
 
 // ---------------------------------------------------------------------------
 // k_score
 // ---------------------------------------------------------------------------
 
-// LDS of k_score: the scan blocks' histograms, or a range block's rho array,
-// which later holds the union bitmap segment and the candidate list.
+// LDS of k_score: the scan blocks' histograms, or a range block's Top-R merge
+// candidates, which later hold the union bitmap segment and the candidate list.
 template <int G>
 struct ScoreLds {
     static constexpr int kScan = G * kHistBins * 4;
-    static constexpr int kRho = 8 * kMaxCache;
+    static constexpr int kRho = 20 * (kMaxCache / kSimSlots) * kMaxR;   // Top-R merge
     static constexpr int kSeg = kSegWords * 4 + kCandList * 4;
     static constexpr int kCand = kRho > kSeg ? kRho : kSeg;
     static constexpr int kBytes = kScan > kCand ? kScan : kCand;
 };
 
-// Scan block: scores of rows [chunk*rows, ...) of KV head (b, g) for the group's
-// exact heads, written to `scores` and counted in the per-head histogram.
+// One contiguous segment [row0, row1) of the rows of KV group (b, g): scores of
+// the group's exact heads (bits of exmask), written to `scores` and counted in
+// each head's histogram.
 template <typename T, int D, int G>
-__device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, unsigned char *lds)
+__device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint32_t exmask,
+                             int64_t row0, int64_t row1, uint32_t *s_hist)
 {
     using R = RowT<T, D>;
-    __shared__ uint32_t s_exmask;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
-    const int chunks = geo.scan_blocks / (a.B * a.Hkv);
-    const int bg = blockIdx.x / chunks, chunk = blockIdx.x % chunks;
-    const int b = bg / a.Hkv, g = bg % a.Hkv;
     const int bh0 = b * a.Hq + g * G;
-
-    if (tid == 0) {
-        uint32_t m = (1u << G) - 1u;
-        if (a.mode == MODE_SELECT) {
-            // Eq. 13: a head is exact iff rho_max < tau (rho_max from k_sim's block maxima).
-            const int nsb = (a.M + kSimSlots - 1) / kSimSlots;
-            m = 0u;
-            for (int j = 0; j < G; ++j) {
-                double mx = -INFINITY;
-                for (int sb = 0; sb < nsb; ++sb)
-                    mx = fmax(mx, w.rho_bmax[(int64_t)(bh0 + j) * (kMaxCache / kSimSlots) + sb]);
-                if (mx < (double)a.tau) m |= 1u << j;
-            }
-        }
-        s_exmask = m;
-    }
-    __syncthreads();
-    const uint32_t exmask = s_exmask;
-    if (exmask == 0) return;
-    const int64_t row0 = (int64_t)chunk * geo.scan_chunk_rows;
-    if (row0 >= a.len) return;
-    if (a.mode == MODE_SELECT && chunk == 0 && tid == 0) atomicAdd(&w.stats[STAT_SCANS], 1ull);
-
-    uint32_t *s_hist = (uint32_t *)lds;
+    if (a.mode == MODE_SELECT && row0 == 0 && tid == 0) atomicAdd(&w.stats[STAT_SCANS], 1ull);
+    __syncthreads();   // the previous segment's histogram flush is done
     for (int i = tid; i < G * kHistBins; i += kScoreThreads) s_hist[i] = 0u;
-    __syncthreads();
-
     uint4 qv[G][R::kNV];
 #pragma unroll
     for (int j = 0; j < G; ++j) {
@@ -361,16 +379,16 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
 #pragma unroll
         for (int s = 0; s < R::kNV; ++s) qv[j][s] = qr[s * 4 + p];
     }
+    __syncthreads();
     const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
-    const int64_t row_end = (row0 + geo.scan_chunk_rows < a.len) ? row0 + geo.scan_chunk_rows : a.len;
 
-    for (int64_t base = row0; base < row_end; base += 2 * kScanRowsPerIter) {
+    for (int64_t base = row0; base < row1; base += 2 * kScanRowsPerIter) {
         uint4 kv[2][R::kNV];
         int64_t row[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             row[u] = base + u * kScanRowsPerIter + wave * 16 + rl;
-            if (row[u] < row_end) {
+            if (row[u] < row1) {
                 const uint4 *rp = (const uint4 *)(kbase + row[u] * D);
 #pragma unroll
                 for (int s = 0; s < R::kNV; ++s) kv[u][s] = rp[s * 4 + p];
@@ -391,7 +409,7 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
             }
             float sc_lo, sc_hi;
             group_scores<G>(acc, p, sc_lo, sc_hi);
-            if (row[u] < row_end) {
+            if (row[u] < row1) {
 #pragma unroll
                 for (int jj = 0; jj < (G + 3) / 4; ++jj) {
                     const int j = jj * 4 + (G == 1 ? 0 : (G == 2 ? (p & 1) : p));
@@ -409,9 +427,77 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
     for (int i = tid; i < G * kHistBins; i += kScoreThreads) {
         const int j = i / kHistBins;
         if ((exmask >> j) & 1u) {
-            uint32_t c = s_hist[i];
+            const uint32_t c = s_hist[i];
             if (c) atomicAdd(&w.hist[(int64_t)(bh0 + j) * kHistBins + (i % kHistBins)], c);
         }
+    }
+}
+
+// Scan block: finds the KV groups that have an exact head (every group outside
+// MODE_SELECT; in MODE_SELECT a head is exact iff rho_max < tau, Eq. 13), and
+// scores its share of the concatenated rows of those groups, so that the scan
+// work spreads over all scan blocks however many groups need it.
+template <typename T, int D, int G>
+__device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, int sbk,
+                           unsigned char *lds)
+{
+    __shared__ uint32_t s_reuse[kMaxHeads / 32];
+    __shared__ int32_t s_glist[kMaxHeads];
+    __shared__ uint32_t s_gmask[kMaxHeads];
+    __shared__ uint32_t s_red[kScoreThreads / 64];
+    constexpr int NT = kScoreThreads;
+    const int tid = threadIdx.x;
+    const int BH = a.B * a.Hq, NG = a.B * a.Hkv;
+    uint32_t *s_hist = (uint32_t *)lds;
+
+    for (int i = tid; i < (BH + 31) / 32; i += NT) s_reuse[i] = 0u;
+    __syncthreads();
+    if (a.mode == MODE_SELECT) {
+        const int nsb = (a.M + kSimSlots - 1) / kSimSlots;
+        for (int t = tid; t < BH * nsb; t += NT) {
+            const int head = t / nsb, sb = t - head * nsb;
+            if (w.rho_bmax[(int64_t)head * (kMaxCache / kSimSlots) + sb] >= (double)a.tau)
+                atomicOr(&s_reuse[head >> 5], 1u << (head & 31));
+        }
+        __syncthreads();
+    }
+    // List of groups with an exact head, in group order.
+    int n_ex = 0;
+    for (int g0 = 0; g0 < NG; g0 += NT) {
+        const int gi = g0 + tid;
+        uint32_t m = 0u;
+        if (gi < NG) {
+            const int head0 = (gi / a.Hkv) * a.Hq + (gi % a.Hkv) * G;
+#pragma unroll
+            for (int j = 0; j < G; ++j) {
+                const int head = head0 + j;
+                if (!((s_reuse[head >> 5] >> (head & 31)) & 1u)) m |= 1u << j;
+            }
+        }
+        uint32_t tot;
+        const uint32_t pos = (uint32_t)n_ex + block_excl_scan<NT>(m != 0u ? 1u : 0u, s_red, &tot);
+        if (m != 0u) {
+            s_glist[pos] = gi;
+            s_gmask[pos] = m;
+        }
+        n_ex += (int)tot;
+    }
+    __syncthreads();
+    if (n_ex == 0) return;
+
+    const int64_t len = a.len;
+    const int64_t total = (int64_t)n_ex * len;
+    int64_t span = (total + geo.scan_blocks - 1) / geo.scan_blocks;
+    span = (span + 2 * kScanRowsPerIter - 1) / (2 * kScanRowsPerIter) * (2 * kScanRowsPerIter);
+    int64_t pos = (int64_t)sbk * span;
+    const int64_t end = pos + span < total ? pos + span : total;
+    while (pos < end) {
+        const int e = (int)(pos / len);
+        const int64_t r0 = pos - (int64_t)e * len;
+        const int64_t r1 = (r0 + (end - pos) < len) ? r0 + (end - pos) : len;
+        const int gi = s_glist[e];
+        scan_segment<T, D, G>(a, w, gi / a.Hkv, gi % a.Hkv, s_gmask[e], r0, r1, s_hist);
+        pos += r1 - r0;
     }
 }
 
@@ -422,25 +508,54 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
 {
     using R = RowT<T, D>;
     constexpr int NT = kScoreThreads;
+    constexpr int kCands = kMaxCache / kSimSlots * kMaxR;   // merge candidates
     __shared__ double s_red64[NT / 64];
     __shared__ uint32_t s_red32[NT / 64];
     __shared__ int32_t s_ret[kMaxR];
+    __shared__ int32_t s_retcnt[kMaxR];
+    static_assert(20 * kCands <= ScoreLds<1>::kCand, "merge candidates fit the range block's LDS");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
     const int bh = cb / kCandRanges, s = cb % kCandRanges;
     const int M = a.M;
     const int n_valid = (int)(a.n_ins < (int64_t)M ? a.n_ins : (int64_t)M);
-    double *s_rho = (double *)lds;
+    const int nsb = (M + kSimSlots - 1) / kSimSlots;
+    const int nret_all = a.R < n_valid ? a.R : n_valid;
+    double *c_rho = (double *)lds;
+    int32_t *c_slot = (int32_t *)(lds + 8 * kCands);
+    int32_t *c_cnt = (int32_t *)(lds + 12 * kCands);
+    int32_t *c_rank = (int32_t *)(lds + 16 * kCands);
+    const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
 
-    // rho of every valid slot (written by k_sim), rho_max and the path (Eq. 13).
-    double mx = -INFINITY;
-    for (int i = tid; i < n_valid; i += NT) {
-        const double r = w.rho[(int64_t)bh * M + i];
-        s_rho[i] = r;
-        mx = fmax(mx, r);
+    // Independent loads first: k_sim block maxima, the blocks' Top-R lists, q.
+    const double bmax_l = w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + (tid < nsb ? tid : 0)];
+    const double bmax = tid < nsb ? bmax_l : -INFINITY;
+    const int per = a.R;                        // list length of a full k_sim block
+    const int nc = nsb * per;
+    for (int c = tid; c < nc; c += NT) {
+        const int sb = c / per, j = c - sb * per;
+        const int nloc = n_valid - sb * kSimSlots;
+        const bool valid = j < (nloc < kSimSlots ? nloc : kSimSlots);
+        const int64_t src = ((int64_t)bh * (kMaxCache / kSimSlots) + sb) * kMaxR + j;
+        const int32_t sl = w.topr[src];
+        const double rr = w.topr_rho[src];
+        const int32_t cn = w.topr_cnt[src];
+        c_slot[c] = valid ? sl : -1;
+        c_rho[c] = valid ? rr : -INFINITY;
+        c_cnt[c] = valid ? cn : 0;
+        c_rank[c] = 0;
     }
-    mx = block_reduce<NT>(mx, s_red64, [](double x, double y) { return fmax(x, y); });
+    uint4 qv[R::kNV];
+    {
+        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)bh * a.q_head_stride);
+#pragma unroll
+        for (int v = 0; v < R::kNV; ++v) qv[v] = qr[v * 4 + p];
+    }
+
+    // rho_max (Eq. 7) and the path (Eq. 13).  block_reduce's barriers also publish
+    // the merge candidates.
+    const double mx = block_reduce<NT>(bmax, s_red64, [](double x, double y) { return fmax(x, y); });
     const int8_t path = mx < (double)a.tau ? PATH_FALLBACK : PATH_REUSE;
-    const int nret = path == PATH_REUSE ? (a.R < n_valid ? a.R : n_valid) : 0;
+    const int nret = path == PATH_REUSE ? nret_all : 0;
     if (s == 0 && tid == 0) {
         w.path[bh] = path;
         if (a.dbg_path) a.dbg_path[bh] = path;
@@ -453,19 +568,34 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
         return;
     }
 
-    // Eq. 7: slot i is the rank-th retrieved entry, rank = number of slots that are
-    // more similar, or equally similar and newer (age (n_ins-1-slot) mod C).
-    const int age0 = (int)(((a.n_ins - 1) % M + M) % M);
-    for (int i = tid; i < n_valid; i += NT) {
-        const double ri = s_rho[i];
-        const int ai = (age0 - i + M) % M;
-        int rank = 0;
-        for (int j = 0; j < n_valid && rank < nret; ++j) {
-            const double rj = s_rho[j];
-            const int aj = (age0 - j + M) % M;
-            rank += (rj > ri || (rj == ri && aj < ai)) ? 1 : 0;
+    // Eq. 7: merge the blocks' Top-R lists.  Candidate c is the rank-th retrieved
+    // entry, rank = number of candidates that are more similar, or equally
+    // similar and newer; P threads share the comparisons of one candidate.
+    {
+        const int age0 = (int)((a.n_ins - 1) % M);
+        int P = 1;
+        while (P * 2 <= 64 && P * 2 * nc <= NT) P *= 2;
+        for (int pair = tid; pair < nc * P; pair += NT) {
+            const int c = pair / P, sub = pair - c * P;
+            const int32_t sl = c_slot[c];
+            if (sl < 0) continue;
+            const double rc = c_rho[c];
+            const int ac = slot_age(age0, sl, M);
+            int cnt = 0;
+            for (int o = sub; o < nc; o += P) {
+                const int32_t so = c_slot[o];
+                cnt += (so >= 0 && better(c_rho[o], slot_age(age0, so, M), rc, ac)) ? 1 : 0;
+            }
+            atomicAdd(&c_rank[c], cnt);
         }
-        if (rank < nret) s_ret[rank] = i;
+    }
+    __syncthreads();
+    for (int c = tid; c < nc; c += NT) {
+        const int rank = c_rank[c];
+        if (c_slot[c] >= 0 && rank < nret) {
+            s_ret[rank] = c_slot[c];
+            s_retcnt[rank] = c_cnt[c];
+        }
     }
     __syncthreads();
     if (s == 0 && a.dbg_ret)
@@ -477,33 +607,45 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     const int64_t lo = (int64_t)s * span;
     const int64_t hi = lo + span < len ? lo + span : len;
     const int64_t w0 = len - a.W > 0 ? len - a.W : 0;
-    uint32_t *bitmap = (uint32_t *)lds;                    // reuses the rho space
+    uint32_t *bitmap = (uint32_t *)lds;                    // reuses the merge space
     int32_t *list = (int32_t *)(lds + kSegWords * 4);
     uint64_t *ents = w.cand_ent + ((int64_t)bh * kCandRanges + s) * a.cand_cap;
-    const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
     const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
-    uint4 qv[R::kNV];
-    {
-        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)bh * a.q_head_stride);
-#pragma unroll
-        for (int v = 0; v < R::kNV; ++v) qv[v] = qr[v * 4 + p];
-    }
-    __syncthreads();   // s_rho is dead from here on
+    __syncthreads();   // the merge candidates are dead from here on
 
     int total = 0;
     for (int64_t seg = lo; seg < hi; seg += (int64_t)kSegWords * 32) {
         const int64_t seg_hi = seg + (int64_t)kSegWords * 32 < hi ? seg + (int64_t)kSegWords * 32 : hi;
         const int nwords = (int)((seg_hi - seg + 31) >> 5);
-        for (int i = tid; i < nwords; i += NT) bitmap[i] = 0u;
-        __syncthreads();
-        for (int r = 0; r < nret; ++r) {
-            const int64_t e = (int64_t)bh * M + s_ret[r];
-            const int32_t *sp = w.supp + e * a.K;
-            const int c = w.cnt[e];
-            for (int t = tid; t < c; t += NT) {
-                const int64_t x = sp[t];
-                if (x >= seg && x < seg_hi) atomicOr(&bitmap[(x - seg) >> 5], 1u << ((x - seg) & 31));
+        // Supports of the retrieved entries: 8 supports' loads in flight before
+        // any bitmap update.
+        for (int t0 = 0; t0 < a.K; t0 += NT) {
+            for (int r0 = 0; r0 < nret; r0 += 8) {
+                // Unconditional loads from clamped (in-bounds) addresses, masked
+                // afterwards, so that all eight are in flight together.
+                int32_t xv[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int r = r0 + u < nret ? r0 + u : 0;
+                    const int t = t0 + tid < a.K ? t0 + tid : 0;
+                    const bool ok = r0 + u < nret && t0 + tid < s_retcnt[r];
+                    const int32_t x = w.supp[((int64_t)bh * M + s_ret[r]) * a.K + t];
+                    xv[u] = ok ? x : -1;
+                }
+                if (t0 == 0 && r0 == 0) {
+                    for (int i = tid; i < nwords; i += NT) bitmap[i] = 0u;
+                    __syncthreads();
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int64_t x = xv[u];
+                    if (x >= seg && x < seg_hi) atomicOr(&bitmap[(x - seg) >> 5], 1u << ((x - seg) & 31));
+                }
             }
+        }
+        if (nret == 0) {
+            for (int i = tid; i < nwords; i += NT) bitmap[i] = 0u;
+            __syncthreads();
         }
         for (int64_t x = (w0 > seg ? w0 : seg) + tid; x < seg_hi; x += NT)
             atomicOr(&bitmap[(x - seg) >> 5], 1u << ((x - seg) & 31));
@@ -560,14 +702,18 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     if (tid == 0) w.cand_cnt[(int64_t)bh * kCandRanges + s] = (uint32_t)total;
 }
 
-template <typename T, int D, int G>
-__global__ __launch_bounds__(kScoreThreads) void k_score(StepArgs a, Ws w, Geometry geo)
+// kSelect: the decode-step variant with range blocks (MODE_SELECT); otherwise
+// every head is exact and the grid holds scan blocks only.
+template <typename T, int D, int G, bool kSelect>
+__global__ __launch_bounds__(kScoreThreads, 4) void k_score(StepArgs a, Ws w, Geometry geo)
 {
     __shared__ __attribute__((aligned(16))) unsigned char lds[ScoreLds<G>::kBytes];
-    if ((int)blockIdx.x < geo.scan_blocks)
-        scan_block<T, D, G>(a, w, geo, lds);
+    // Range blocks (latency-bound) come first so they are dispatched before the
+    // bandwidth-bound scan blocks.
+    if (kSelect && (int)blockIdx.x < geo.cand_blocks)
+        range_block<T, D>(a, w, (int)blockIdx.x, lds);
     else
-        range_block<T, D>(a, w, (int)blockIdx.x - geo.scan_blocks, lds);
+        scan_block<T, D, G>(a, w, geo, (int)blockIdx.x - (kSelect ? geo.cand_blocks : 0), lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -633,14 +779,14 @@ template <int D, int NT>
 struct FinalSmem {
     uint64_t ent[kEntCache];        // the head's entries in index order, when they fit
     uint64_t sel[kMaxK];            // selected (index << 32 | score key), index order
-    float wgt[kMaxK];
     uint32_t pref[kMaxRegions + 1]; // region prefix counts
     uint32_t hist[kHistBins];
     float part[NT / 64][D / kFinalSlices];
+    float lpart[NT / 64];
     float qbar[D];
     double red64[NT / 64];
-    float red32[NT / 64];
     uint32_t redu[NT / 64];
+    unsigned long long rmax, rmin;
     uint32_t found_digit, found_above, found_cnt;
 };
 
@@ -652,20 +798,22 @@ struct Regions {
     const uint64_t *staged;   // LDS copy or nullptr
     const uint32_t *pref;
     int nreg;
+    int top;                  // largest power of two below nreg (0 if nreg == 1)
     __device__ uint64_t get(int j) const
     {
         if (staged) return staged[j];
-        int lo = 0, hi = nreg - 1;   // last region r with pref[r] <= j
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if ((int)pref[mid] <= j) lo = mid; else hi = mid - 1;
+        int lo = 0;           // last region r with pref[r] <= j (empty regions skipped)
+        for (int step = top; step > 0; step >>= 1) {
+            const int c = lo + step;
+            if (c < nreg && (int)pref[c] <= j) lo = c;
         }
         return base[(int64_t)lo * stride + (j - (int)pref[lo])];
     }
 };
 
 // Radix select over distinct 64-bit ranks with 11-bit digits, most significant
-// first.  On return the top min(K, n) entries are exactly those with
+// first, starting at the highest bit in which the ranks differ (rmax ^ rmin).
+// On return the top min(K, n) entries are exactly those with
 // (rank & mask) >= prefix (mask == 0 selects everything).
 template <int D, int NT>
 __device__ void radix_threshold(const Regions &rg, int K, FinalSmem<D, NT> &sm, uint64_t &prefix,
@@ -675,10 +823,16 @@ __device__ void radix_threshold(const Regions &rg, int K, FinalSmem<D, NT> &sm, 
     prefix = 0;
     mask = 0;
     if (rg.n <= K) return;
+    const uint64_t diff = (uint64_t)sm.rmax ^ (uint64_t)sm.rmin;   // nonzero: ranks are distinct
+    const int hb = 63 - __clzll((long long)diff);
+    if (hb < 63) {
+        mask = ~0ull << (hb + 1);
+        prefix = (uint64_t)sm.rmax & mask;
+    }
     uint32_t k_rem = (uint32_t)K;
-    for (int shift = 53; ; shift -= 11) {
-        const int sh = shift > 0 ? shift : 0;
-        const int width = shift > 0 ? 11 : 11 + shift;
+    for (int top = hb; top >= 0; top -= 11) {
+        const int width = top + 1 < 11 ? top + 1 : 11;
+        const int sh = top + 1 - width;
         const uint32_t nb = 1u << width;
         for (uint32_t i = tid; i < nb; i += NT) sm.hist[i] = 0u;
         __syncthreads();
@@ -725,7 +879,9 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     constexpr int LPR = SB / 16;                         // lanes per slice row
     constexpr int RPW = 64 / LPR;                        // rows per wave instruction
     constexpr int EPV = 16 / (int)sizeof(T);
+    constexpr int kRegPerThread = kMaxRegions / NT;
     static_assert(SB % 16 == 0 && LPR >= 1 && LPR <= 64, "slice geometry");
+    static_assert(kMaxRegions % NT == 0 && kCandRanges <= NT, "region ownership");
     __shared__ FinalSmem<D, NT> sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int bh = blockIdx.x / kFinalSlices, slice = blockIdx.x % kFinalSlices;
@@ -741,45 +897,100 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
         if (a.dbg_ret)
             for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = -1;
     }
-    const bool reuse = a.mode == MODE_SELECT && w.path[bh] == PATH_REUSE;
 
-    // Region layout of this head's entries.
+    // Path and the region counts of both layouts in one round trip.
+    const int nreg_s = (int)((a.len + kFilterRows - 1) / kFilterRows);
+    const int rpt = (nreg_s + NT - 1) / NT;
+    uint32_t scnt[kRegPerThread];
+#pragma unroll
+    for (int u = 0; u < kRegPerThread; ++u) {
+        const int r = tid * rpt + u;
+        const bool ok = u < rpt && r < nreg_s;
+        const uint32_t x = w.surv_cnt[(int64_t)bh * a.n_regions + (ok ? r : 0)];
+        scnt[u] = ok ? x : 0u;
+    }
+    const bool sel_mode = a.mode == MODE_SELECT;
+    const uint32_t ccnt_l = w.cand_cnt[(int64_t)bh * kCandRanges + (tid < kCandRanges ? tid : 0)];
+    const uint32_t ccnt = (sel_mode && tid < kCandRanges) ? ccnt_l : 0u;
+    const bool reuse = sel_mode && w.path[bh] == PATH_REUSE;
+
     Regions rg;
-    const uint32_t *cnts;
     if (reuse) {
         rg.base = w.cand_ent + (int64_t)bh * kCandRanges * a.cand_cap;
         rg.stride = a.cand_cap;
         rg.nreg = kCandRanges;
-        cnts = w.cand_cnt + (int64_t)bh * kCandRanges;
     } else {
         rg.base = w.surv + (int64_t)bh * a.row_stride;
         rg.stride = kFilterRows;
-        rg.nreg = (int)((a.len + kFilterRows - 1) / kFilterRows);
-        cnts = w.surv_cnt + (int64_t)bh * a.n_regions;
+        rg.nreg = nreg_s;
     }
     {
-        // prefix over region counts: thread t owns regions [t*rpt, ...)
-        const int rpt = (rg.nreg + NT - 1) / NT;
-        const int r0 = tid * rpt < rg.nreg ? tid * rpt : rg.nreg;
-        const int r1 = r0 + rpt < rg.nreg ? r0 + rpt : rg.nreg;
         uint32_t mine = 0;
-        for (int r = r0; r < r1; ++r) mine += cnts[r];
+        if (reuse) {
+            mine = ccnt;
+        } else {
+#pragma unroll
+            for (int u = 0; u < kRegPerThread; ++u) mine += scnt[u];
+        }
         uint32_t total;
         uint32_t run = block_excl_scan<NT>(mine, sm.redu, &total);
-        for (int r = r0; r < r1; ++r) {
-            sm.pref[r] = run;
-            run += cnts[r];
+        if (reuse) {
+            if (tid < kCandRanges) sm.pref[tid] = run;
+        } else {
+#pragma unroll
+            for (int u = 0; u < kRegPerThread; ++u) {
+                const int r = tid * rpt + u;
+                if (u < rpt && r < nreg_s) {
+                    sm.pref[r] = run;
+                    run += scnt[u];
+                }
+            }
         }
-        if (tid == 0) sm.pref[rg.nreg] = total;
+        if (tid == 0) {
+            sm.pref[rg.nreg] = total;
+            sm.rmax = 0ull;
+            sm.rmin = ~0ull;
+        }
         __syncthreads();
         rg.n = (int)total;
     }
     rg.pref = sm.pref;
     rg.staged = nullptr;
-    if (rg.n <= kEntCache) {
-        for (int j = tid; j < rg.n; j += NT) sm.ent[j] = rg.get(j);
+    rg.top = rg.nreg > 1 ? 1 << (31 - __clz(rg.nreg - 1)) : 0;
+    {
+        // Stage the entries (in index order) and find the largest and smallest rank.
+        uint64_t lmax = 0ull, lmin = ~0ull;
+        const bool stage = rg.n <= kEntCache;
+        for (int j0 = 0; j0 < rg.n; j0 += 4 * NT) {
+            uint64_t e[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int j = j0 + u * NT + tid;
+                e[u] = rg.get(j < rg.n ? j : 0);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int j = j0 + u * NT + tid;
+                if (j < rg.n) {
+                    if (stage) sm.ent[j] = e[u];
+                    lmax = e[u] > lmax ? e[u] : lmax;
+                    lmin = e[u] < lmin ? e[u] : lmin;
+                }
+            }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            const uint64_t omax = __shfl_xor((unsigned long long)lmax, o);
+            const uint64_t omin = __shfl_xor((unsigned long long)lmin, o);
+            lmax = omax > lmax ? omax : lmax;
+            lmin = omin < lmin ? omin : lmin;
+        }
+        if (lane == 0) {
+            atomicMax(&sm.rmax, (unsigned long long)lmax);
+            atomicMin(&sm.rmin, (unsigned long long)lmin);
+        }
         __syncthreads();
-        rg.staged = sm.ent;
+        if (stage) rg.staged = sm.ent;
     }
 
     // Top-K (Eq. 1 / Eq. 11), then the selected entries in index order.
@@ -803,42 +1014,44 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     }
 
     if (writes_out) {
-        // Eq. 12 on this block's slice of the head dimension.
-        float mx = -INFINITY;
-        for (int t = tid; t < kn; t += NT) mx = fmaxf(mx, key_score((uint32_t)sm.sel[t]));
-        mx = block_reduce<NT>(mx, sm.red32, [](float x, float y) { return fmaxf(x, y); });
-        float lsum = 0.0f;
-        for (int t = tid; t < kn; t += NT) {
-            const float wt = expf(key_score((uint32_t)sm.sel[t]) - mx);
-            sm.wgt[t] = wt;
-            lsum += wt;
-        }
-        lsum = block_reduce<NT>(lsum, sm.red32, [](float x, float y) { return x + y; });
+        // Eq. 12 on this block's slice of the head dimension; the largest selected
+        // score is the top rank's.
+        const float mx = key_score(rank_key((uint64_t)sm.rmax));
         const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
         const T *vbase = (const T *)a.v + ((int64_t)b * a.Hkv + g) * a.max_len * D + slice * DS;
         const int sub = lane / LPR, vl = lane % LPR;
         float acc[EPV];
 #pragma unroll
         for (int e = 0; e < EPV; ++e) acc[e] = 0.0f;
+        float lsum = 0.0f;
 #pragma unroll 4
         for (int t = wave * RPW + sub; t < kn; t += NW * RPW) {
-            const uint32_t idx = (uint32_t)(sm.sel[t] >> 32);
-            const uint4 raw = ((const uint4 *)(vbase + (int64_t)idx * D))[vl];
-            Dot<T>::axpy(raw, sm.wgt[t], acc);
+            const uint64_t se = sm.sel[t];
+            const uint4 raw = ((const uint4 *)(vbase + (int64_t)(uint32_t)(se >> 32) * D))[vl];
+            const float wt = expf(key_score((uint32_t)se) - mx);
+            Dot<T>::axpy(raw, wt, acc);
+            lsum += vl == 0 ? wt : 0.0f;
         }
 #pragma unroll
-        for (int o = LPR; o < 64; o <<= 1)
+        for (int o = LPR; o < 64; o <<= 1) {
 #pragma unroll
             for (int e = 0; e < EPV; ++e) acc[e] += __shfl_xor(acc[e], o);
-        if (sub == 0)
+            lsum += __shfl_xor(lsum, o);
+        }
+        if (sub == 0) {
 #pragma unroll
             for (int e = 0; e < EPV; ++e) sm.part[wave][vl * EPV + e] = acc[e];
+            if (vl == 0) sm.lpart[wave] = lsum;
+        }
         __syncthreads();
         if (tid < DS) {
-            float o = 0.0f;
+            float o = 0.0f, l = 0.0f;
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) o += sm.part[ww][tid];
-            a.out[(int64_t)bh * D + slice * DS + tid] = kn > 0 ? o / lsum : 0.0f;
+            for (int ww = 0; ww < NW; ++ww) {
+                o += sm.part[ww][tid];
+                l += sm.lpart[ww];
+            }
+            a.out[(int64_t)bh * D + slice * DS + tid] = kn > 0 ? o / l : 0.0f;
         }
     }
     if (slice != 0) return;
@@ -910,7 +1123,9 @@ static hipError_t score_impl(const StepArgs &a, const Ws &w, const Geometry &geo
                              const Timing &tm)
 {
     const int blocks = geo.scan_blocks + geo.cand_blocks;
-    return launch(k_score<T, D, G>, dim3((unsigned)blocks), dim3(kScoreThreads), s, tm, a, w, geo);
+    if (a.mode == MODE_SELECT)
+        return launch(k_score<T, D, G, true>, dim3((unsigned)blocks), dim3(kScoreThreads), s, tm, a, w, geo);
+    return launch(k_score<T, D, G, false>, dim3((unsigned)blocks), dim3(kScoreThreads), s, tm, a, w, geo);
 }
 
 template <typename T, int D>
