@@ -19,6 +19,7 @@ from the library's own event profiling over the timed steps.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import platform
@@ -31,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+COPY_BYTES = 256 << 20
 METRIC = "µs per decode step (all heads) + speedup vs Exact Top-K, 128K ctx, K=512"
 
 
@@ -43,9 +45,14 @@ def parse():
     ap.add_argument("--warm", action="store_true", help="no cache flush between steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--profile-kernels", type=int, default=0,
-                    help="record HIP events around every kernel in the timed steps "
-                         "(adds several us per launch to the step times)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the passes, run a plain 256 MiB device copy 8 times, so that "
+                         "a hardware-counter run can scale FETCH_SIZE / WRITE_SIZE by what "
+                         "they read for a copy of known size")
+    ap.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+                    help="no GPU work: turn the csv output of a rocprofv3 kernel-trace run and "
+                         "of a FETCH_SIZE and a WRITE_SIZE counter run of this script (with "
+                         "--copy-calibration) into the text summaries under profiles/")
     return ap.parse_args()
 
 
@@ -55,6 +62,9 @@ def log(*a):
 
 def main():
     args = parse()
+    if args.summarize:
+        summarize(args, *args.summarize)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); the "
               "multi-GPU layout is a design note only", file=sys.stderr)
@@ -167,32 +177,45 @@ def main():
     step_gbs = retopk_bytes / K_steps / (r_us * 1e-6) / 1e9
     exact_gbs = exact_bytes / K_steps / (e_us * 1e-6) / 1e9
 
-    # Dominant kernel of the ReTopK step and its algorithmic bytes per launch.
+    # Dominant kernel of the ReTopK pass and its algorithmic bytes per launch: the
+    # bytes the method has to read for the heads that launch serves (key rows
+    # scanned or gathered, cached queries, support lists, value rows); buffers
+    # internal to this implementation (scores, survivor lists) are not counted.
+    # Refresh steps run every head as a full scan (retopk_scan); the other steps
+    # launch retopk_sim and retopk_score.
+    refresh_steps = refresh // BH if BH else 0
+    select_steps = K_steps - refresh_steps
+    scans_select = scans - refresh_steps * w.batch * w.n_kv_heads
     roof = None
     if r_prof:
         dom = max(r_prof, key=lambda n: r_prof[n][1])
         launches, tot_ms = r_prof[dom]
         if dom == "retopk_score":
-            kbytes = scans * mean_len * d * e + cand_sum * d * e + reuse * d * e
+            kbytes = (scans_select * mean_len * d * e + cand_sum * d * e
+                      + reuse * w.r * w.k * 4 + select_steps * BH * d * e)
         elif dom == "retopk_sim":
-            kbytes = (reuse + fallback) * (C_valid * d * 4 + d * e) + reuse * w.r * w.k * 4
+            kbytes = select_steps * BH * (C_valid * d * 4 + d * e)
         elif dom == "retopk_final":
             kbytes = head_steps * (w.k * d * e + d * 4)
+        elif dom == "retopk_scan":
+            kbytes = refresh_steps * w.batch * w.n_kv_heads * mean_len * d * e
         else:
             kbytes = exact_heads * mean_len * 4
         ach = kbytes / launches / (tot_ms / launches * 1e-3) / 1e9
         roof = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
-                "traffic": None,
+                "traffic": traffic_per_launch(dom, w.name),
                 "avg_launch_us": round(tot_ms / launches * 1e3, 2), "launches": launches,
                 "bytes_per_launch": round(kbytes / launches)}
     exact_roof = None
-    if e_prof and "retopk_score" in e_prof:
-        launches, tot_ms = e_prof["retopk_score"]
+    if e_prof and e_prof.get("retopk_scan", (0, 0))[0]:
+        launches, tot_ms = e_prof["retopk_scan"]
         scan_bytes = K_steps * w.batch * w.n_kv_heads * mean_len * d * e
         ach = scan_bytes / (tot_ms * 1e-3) / 1e9
-        exact_roof = {"kernel": "retopk_score (full scan)", "achieved": round(ach, 1),
-                      "frac": round(ach / HBM_PEAK_GBS, 4),
+        exact_roof = {"kernel": "retopk_scan", "bound": "hbm", "achieved": round(ach, 1),
+                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                      "traffic": traffic_per_launch("retopk_scan", w.name),
+                      "bytes_per_launch": round(scan_bytes / launches),
                       "avg_launch_us": round(tot_ms / launches * 1e3, 2)}
 
     # ---- CPU baseline: the oracle on a bounded sample ------------------------
@@ -242,6 +265,41 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
+    if args.copy_calibration:
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(8):
+            sink.add_(flush.sum())
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copy calibration: 8 x {COPY_BYTES} bytes")
+
+
+def kernel_source_digest() -> str:
+    path = os.path.join(ROOT, "paper_2607_27692_amd", "csrc", "retopk_kernels.hip")
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_per_launch(kernel: str, workload: str):
+    """Measured HBM bytes per launch of `kernel` (FETCH_SIZE + WRITE_SIZE, scaled
+    by a copy of known size), from the counter summary kept under profiles/;
+    None when there is none or the kernel source has changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                key, val = line.split(":", 1)
+                fields[key.strip()] = val.strip()
+    if fields.get("kernel_source_sha256") != kernel_source_digest():
+        return None
+    try:
+        return int(float(fields["traffic_bytes_per_launch"]))
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(w, inp, seconds: float):
@@ -284,6 +342,145 @@ def cpu_baseline(w, inp, seconds: float):
                        f"0, {n_st} ReTopK steps from a seeded cache state and {n_ex} Exact "
                        f"Top-K steps, scaled x{scale:g} to all heads"),
             "cpu": platform.processor() or platform.machine()}
+
+
+# ---- profiler summaries -------------------------------------------------------
+SYMBOLS = {  # kernel symbol prefix -> name used by the library's own profiling
+    "void retopk::k_sim<": "retopk_sim",
+    "void retopk::k_score<unsigned short, 128, 4, true>": "retopk_score",
+    "void retopk::k_score<unsigned short, 128, 4, false>": "retopk_scan",
+    "retopk::k_filter(": "retopk_filter",
+    "void retopk::k_final<": "retopk_final",
+}
+
+
+def _lib_name(symbol: str):
+    for prefix, name in SYMBOLS.items():
+        if symbol.startswith(prefix):
+            return name
+    return None
+
+
+def _read_csv(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _passes(names, w, steps, warmup):
+    """Splits the library's dispatches (in dispatch order) into the bench's
+    passes.  Every pass starts on a fresh handle whose prefill issues one
+    scan, filter, final triple per prompt-tail query; a decode step that selects
+    issues sim, score, filter, final, any other step scan, filter, final.
+    Returns (label, first, end) positions of each pass's step dispatches."""
+    plan = [("warm-up", 2 * min(warmup, w.steps)), ("retopk timed", steps),
+            ("exact timed", steps), ("retopk profiled", steps), ("exact profiled", steps)]
+    step4 = ["retopk_sim", "retopk_score", "retopk_filter", "retopk_final"]
+    step3 = ["retopk_scan", "retopk_filter", "retopk_final"]
+    out, i = [], 0
+    for label, n_steps in plan:
+        for _ in range(w.cache_cap):
+            assert names[i:i + 3] == step3, f"unexpected prefill dispatches at {i}"
+            i += 3
+        start = i
+        for _ in range(n_steps):
+            n = 4 if names[i] == "retopk_sim" else 3
+            assert names[i:i + n] == (step4 if n == 4 else step3), f"unexpected step at {i}"
+            i += n
+        out.append((label, start, i))
+    assert i == len(names), "dispatches left over"
+    return out
+
+
+def summarize(args, trace_dir, fetch_dir, write_dir):
+    import glob
+    from paper_2607_27692_amd.inputs import WORKLOADS
+    w = WORKLOADS[args.workload]
+    steps = min(args.steps, w.steps)
+    trace = _read_csv(glob.glob(os.path.join(trace_dir, "*kernel_trace.csv"))[0])
+    stats = _read_csv(glob.glob(os.path.join(trace_dir, "*kernel_stats.csv"))[0])
+    trace.sort(key=lambda r: int(r["Dispatch_Id"]))
+    lib = [(r, _lib_name(r["Kernel_Name"])) for r in trace]
+    lib = [(r, n) for r, n in lib if n]
+    names = [n for _, n in lib]
+    passes = _passes(names, w, steps, args.warmup)
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3  # noqa: E731
+
+    lines = [f"# Kernel durations, {w.name} workload, rocprofv3 kernel trace",
+             "command: cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats -f csv "
+             "-d <out>/kt -o kt -- python3 -u <repo>/bench.py --no-cpu-baseline",
+             "summary: python bench.py --summarize <out>/kt <out>/pmc_fetch <out>/pmc_write",
+             "",
+             "## rocprofv3 --stats (every dispatch of the run: prefill, warm-up and the four passes)",
+             f"{'kernel':60s} {'library name':14s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'share':>7s}"]
+    for r in stats:
+        name = _lib_name(r["Name"]) or ""
+        lines.append(f"{r['Name'][:60]:60s} {name:14s} {int(r['Calls']):6d} "
+                     f"{float(r['AverageNs']) / 1e3:9.2f} {float(r['MinNs']) / 1e3:9.2f} "
+                     f"{float(r['MaxNs']) / 1e3:9.2f} {float(r['Percentage']):6.2f}%")
+    lines += ["", f"## per pass, decode-step dispatches only ({steps} steps per pass)",
+              f"{'pass':18s} {'kernel':14s} {'launches':>8s} {'avg_us':>9s}"]
+    for label, a, b in passes:
+        acc = {}
+        for r, n in lib[a:b]:
+            acc.setdefault(n, []).append(dur(r))
+        for n in ("retopk_sim", "retopk_score", "retopk_scan", "retopk_filter", "retopk_final"):
+            if n in acc:
+                v = acc[n]
+                lines.append(f"{label:18s} {n:14s} {len(v):8d} {sum(v) / len(v):9.2f}")
+    kt_path = os.path.join(ROOT, "profiles", f"kernels_{w.name}.txt")
+
+    # ---- counters: FETCH_SIZE / WRITE_SIZE, scaled by the copy calibration ----
+    def counters(d):
+        rows = _read_csv(glob.glob(os.path.join(d, "*counter_collection.csv"))[0])
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        libr = [(float(r["Counter_Value"]), _lib_name(r["Kernel_Name"])) for r in rows]
+        copies = [float(r["Counter_Value"]) for r in rows
+                  if r["Kernel_Name"].startswith("__amd_rocclr_copyBuffer")]
+        return [(v, n) for v, n in libr if n], copies
+    fetch, fcopy = counters(fetch_dir)
+    write, wcopy = counters(write_dir)
+    assert [n for _, n in fetch] == names == [n for _, n in write], "dispatch sequences differ"
+    copy_kib = COPY_BYTES / 1024
+    f_big = [v for v in fcopy if v > copy_kib / 4]
+    w_big = [v for v in wcopy if v > copy_kib / 4]
+    f_factor = copy_kib / (sum(f_big) / len(f_big))
+    w_factor = copy_kib / (sum(w_big) / len(w_big))
+    digest = kernel_source_digest()
+    written = [kt_path]
+    for kernel, pass_idx in (("retopk_score", 1), ("retopk_scan", 2)):
+        _, a, b = passes[pass_idx]
+        fv = [v for v, n in fetch[a:b] if n == kernel]
+        wv = [v for v, n in write[a:b] if n == kernel]
+        fk, wk = sum(fv) / len(fv), sum(wv) / len(wv)
+        traffic = (fk * f_factor + wk * w_factor) * 1024
+        out = [f"# HBM traffic per launch of {kernel}, {w.name} workload, rocprofv3 counters",
+               "command_fetch: cd /tmp && export TMPDIR=/tmp && timeout -s KILL 300 rocprofv3 "
+               "--pmc FETCH_SIZE -f csv -d <out>/pmc_fetch -o pmc -- python3 -u <repo>/bench.py "
+               "--no-cpu-baseline --copy-calibration",
+               "command_write: the same with --pmc WRITE_SIZE -d <out>/pmc_write",
+               "summary: python bench.py --summarize <out>/kt <out>/pmc_fetch <out>/pmc_write",
+               f"copy_bytes: {COPY_BYTES}",
+               f"copy_fetch_kib: {sum(f_big) / len(f_big):.1f}",
+               f"copy_write_kib: {sum(w_big) / len(w_big):.1f}",
+               f"fetch_factor: {f_factor:.4f}",
+               f"write_factor: {w_factor:.4f}",
+               f"pass: {passes[pass_idx][0]} (first timed pass)",
+               f"launches: {len(fv)}",
+               f"fetch_kib_per_launch: {fk:.1f}",
+               f"write_kib_per_launch: {wk:.1f}",
+               f"traffic_bytes_per_launch: {traffic:.0f}",
+               f"kernel_source_sha256: {digest}"]
+        path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{w.name}.txt")
+        with open(path, "w") as f:
+            f.write("\n".join(out) + "\n")
+        written.append(path)
+        lines.append(f"traffic {kernel}: {traffic / 1e6:.2f} MB per launch "
+                     f"(fetch {fk:.0f} KiB x {f_factor:.3f}, write {wk:.0f} KiB x {w_factor:.3f})")
+    with open(kt_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    for p_ in written:
+        log(f"[bench] wrote {p_}")
 
 
 if __name__ == "__main__":

@@ -151,12 +151,19 @@ retopk_status retopk_get_state(retopk_handle h, float *qbar, int32_t *supp, int3
 retopk_status retopk_set_state(retopk_handle h, const float *qbar, const int32_t *supp,
                                const int32_t *cnt, int64_t n_inserted, int64_t t_dec);
 
-/* Per-kernel timing with HIP events recorded around each launch, on the launch
- * stream.  retopk_profile(h, 1) clears and starts recording, retopk_profile(h, 0)
- * stops.  retopk_profile_read (synchronises) fills, for kernel ids
- * 0 .. n_kernels-1 (see retopk_kernel_name), the number of launches and their
- * summed duration in milliseconds; it returns RETOPK_ERR_STATE if more launches
- * were recorded than the event pool holds (65536). */
+/* Per-kernel timing with HIP events attached to each kernel's dispatch, on the
+ * launch stream.  retopk_profile(h, 1) clears and starts recording,
+ * retopk_profile(h, 0) stops.  retopk_profile_read (synchronises) fills, for
+ * kernel ids 0 .. n_kernels-1, the number of launches and their summed duration
+ * in milliseconds; it returns RETOPK_ERR_STATE if more launches were recorded
+ * than the event pool holds (65536).  Kernel ids, in the order of a step:
+ *   0 retopk_sim     query-cache similarities and Top-R (decode steps that select)
+ *   1 retopk_score   candidate gathering and scoring plus the full-history scans
+ *                    of fallback heads (decode steps that select)
+ *   2 retopk_scan    the scoring kernel when every head scans its full history
+ *                    (refresh, cold, Exact Top-K, prefill)
+ *   3 retopk_filter  threshold bucket and survivor compaction
+ *   4 retopk_final   exact Top-K, Softmax-V, cache insert */
 retopk_status retopk_profile(retopk_handle h, int32_t enable);
 retopk_status retopk_profile_read(retopk_handle h, int32_t n_kernels, uint64_t *launches,
                                   double *total_ms);

@@ -15,10 +15,13 @@ using namespace retopk;
 namespace {
 
 constexpr int kProfileMaxLaunches = 65536;
-constexpr int kNumKernels = 4;
-const char *const kKernelNames[kNumKernels] = {"retopk_sim", "retopk_score", "retopk_filter",
-                                               "retopk_final"};
-enum { KID_SIM = 0, KID_SCORE = 1, KID_FILTER = 2, KID_FINAL = 3 };
+constexpr int kNumKernels = 5;
+// retopk_score is the scoring kernel of a decode step that selects (candidate
+// blocks beside the scans of fallback heads); retopk_scan is the same kernel
+// built for steps where every head takes the full-history scan.
+const char *const kKernelNames[kNumKernels] = {"retopk_sim", "retopk_score", "retopk_scan",
+                                               "retopk_filter", "retopk_final"};
+enum { KID_SIM = 0, KID_SCORE = 1, KID_SCAN = 2, KID_FILTER = 3, KID_FINAL = 4 };
 
 }  // namespace
 
@@ -165,7 +168,7 @@ retopk_status run_step(retopk_handle h, const StepArgs &a, int mode, hipStream_t
         if ((st = timing_for(h, KID_SIM, &tm)) != RETOPK_OK) return st;
         if (launch_sim(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
     }
-    if ((st = timing_for(h, KID_SCORE, &tm)) != RETOPK_OK) return st;
+    if ((st = timing_for(h, mode == MODE_SELECT ? KID_SCORE : KID_SCAN, &tm)) != RETOPK_OK) return st;
     if (launch_score(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
     if ((st = timing_for(h, KID_FILTER, &tm)) != RETOPK_OK) return st;
     if (launch_filter(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);

@@ -37,8 +37,9 @@ def test_every_declared_symbol_is_exported(lib):
 def test_status_strings(lib):
     for code in (0, -1, -2, -3, -4, -5):
         assert R.retopk_status_string(code) == R.STATUS[code]
-    assert [R.retopk_kernel_name(i) for i in range(4)] == ["retopk_sim", "retopk_score", "retopk_filter", "retopk_final"]
-    assert R.retopk_kernel_name(99) is None
+    assert [R.retopk_kernel_name(i) for i in range(5)] == [
+        "retopk_sim", "retopk_score", "retopk_scan", "retopk_filter", "retopk_final"]
+    assert R.retopk_kernel_name(5) is None and R.retopk_kernel_name(-1) is None
 
 
 def _cfg(**kw):
