@@ -348,16 +348,15 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
 // k_score
 // ---------------------------------------------------------------------------
 
-// LDS of k_score: the scan blocks' histograms, or a range block's Top-R merge
-// candidates, which later hold the union bitmap segment and the candidate list.
-template <int G>
-struct ScoreLds {
-    static constexpr int kScan = G * kHistBins * 4;
-    static constexpr int kRho = 20 * (kMaxCache / kSimSlots) * kMaxR;   // Top-R merge
-    static constexpr int kSeg = kSegWords * 4 + kCandList * 4;
-    static constexpr int kCand = kRho > kSeg ? kRho : kSeg;
-    static constexpr int kBytes = kScan > kCand ? kScan : kCand;
-};
+// Dynamic LDS of k_score (bytes): the scan blocks' histograms, or a range
+// block's Top-R merge candidates (20 bytes each), which later hold the union
+// bitmap segment and the candidate list.
+__host__ __device__ constexpr int score_scan_lds(int g) { return g * kHistBins * 4; }
+__host__ __device__ constexpr int score_range_lds(int n_merge)
+{
+    return 20 * n_merge > kSegWords * 4 + kCandList * 4 ? 20 * n_merge : kSegWords * 4 + kCandList * 4;
+}
+constexpr int kLocalGroups = 512;   // exact KV groups one scan block's rows can touch
 
 // One contiguous segment [row0, row1) of the rows of KV group (b, g): scores of
 // the group's exact heads (bits of exmask), written to `scores` and counted in
@@ -433,26 +432,45 @@ __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint3
     }
 }
 
-// Scan block: finds the KV groups that have an exact head (every group outside
-// MODE_SELECT; in MODE_SELECT a head is exact iff rho_max < tau, Eq. 13), and
-// scores its share of the concatenated rows of those groups, so that the scan
-// work spreads over all scan blocks however many groups need it.
-template <typename T, int D, int G>
+// Scan block sbk: scores its share of the concatenated rows of the KV groups that
+// have an exact head, so that the scan work spreads over all scan blocks however
+// many groups need it.  Outside MODE_SELECT every group is exact; in MODE_SELECT
+// a head is exact iff rho_max < tau (Eq. 13), read from the k_sim block maxima.
+template <typename T, int D, int G, bool kSelect>
 __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, int sbk,
                            unsigned char *lds)
 {
-    __shared__ uint32_t s_reuse[kMaxHeads / 32];
-    __shared__ int32_t s_glist[kMaxHeads];
-    __shared__ uint32_t s_gmask[kMaxHeads];
-    __shared__ uint32_t s_red[kScoreThreads / 64];
     constexpr int NT = kScoreThreads;
     const int tid = threadIdx.x;
-    const int BH = a.B * a.Hq, NG = a.B * a.Hkv;
+    const int NG = a.B * a.Hkv;
+    const int64_t len = a.len;
     uint32_t *s_hist = (uint32_t *)lds;
-
-    for (int i = tid; i < (BH + 31) / 32; i += NT) s_reuse[i] = 0u;
-    __syncthreads();
-    if (a.mode == MODE_SELECT) {
+    auto do_span = [&](int n_ex, auto group_of) {
+        const int64_t total = (int64_t)n_ex * len;
+        int64_t span = (total + geo.scan_blocks - 1) / geo.scan_blocks;
+        span = (span + 2 * kScanRowsPerIter - 1) / (2 * kScanRowsPerIter) * (2 * kScanRowsPerIter);
+        int64_t pos = (int64_t)sbk * span;
+        const int64_t end = pos + span < total ? pos + span : total;
+        while (pos < end) {
+            const int e = (int)(pos / len);
+            const int64_t r0 = pos - (int64_t)e * len;
+            const int64_t r1 = (r0 + (end - pos) < len) ? r0 + (end - pos) : len;
+            int gi;
+            uint32_t m;
+            group_of(e, gi, m);
+            scan_segment<T, D, G>(a, w, gi / a.Hkv, gi % a.Hkv, m, r0, r1, s_hist);
+            pos += r1 - r0;
+        }
+    };
+    if constexpr (!kSelect) {
+        do_span(NG, [](int e, int &gi, uint32_t &m) { gi = e; m = (1u << G) - 1u; });
+    } else {
+        __shared__ uint32_t s_reuse[kMaxHeads / 32];
+        __shared__ uint32_t s_local[kLocalGroups];   // group * 256 + exact-head mask
+        __shared__ uint32_t s_red[NT / 64];
+        const int BH = a.B * a.Hq;
+        for (int i = tid; i < (BH + 31) / 32; i += NT) s_reuse[i] = 0u;
+        __syncthreads();
         const int nsb = (a.M + kSimSlots - 1) / kSimSlots;
         for (int t = tid; t < BH * nsb; t += NT) {
             const int head = t / nsb, sb = t - head * nsb;
@@ -460,44 +478,63 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
                 atomicOr(&s_reuse[head >> 5], 1u << (head & 31));
         }
         __syncthreads();
-    }
-    // List of groups with an exact head, in group order.
-    int n_ex = 0;
-    for (int g0 = 0; g0 < NG; g0 += NT) {
-        const int gi = g0 + tid;
-        uint32_t m = 0u;
-        if (gi < NG) {
+        auto mask_of = [&](int gi) {
+            uint32_t m = 0u;
             const int head0 = (gi / a.Hkv) * a.Hq + (gi % a.Hkv) * G;
 #pragma unroll
             for (int j = 0; j < G; ++j) {
                 const int head = head0 + j;
                 if (!((s_reuse[head >> 5] >> (head & 31)) & 1u)) m |= 1u << j;
             }
+            return m;
+        };
+        // Pass 1: the number of exact groups, hence this block's rows (with at
+        // most NT groups, one pass also ranks them).
+        int n_ex = 0;
+        uint32_t m0 = 0u;
+        int e0 = 0;
+        for (int g0 = 0; g0 < NG; g0 += NT) {
+            const int gi = g0 + tid;
+            const uint32_t m = gi < NG ? mask_of(gi) : 0u;
+            uint32_t tot;
+            const int e = n_ex + (int)block_excl_scan<NT>(m != 0u ? 1u : 0u, s_red, &tot);
+            if (g0 == 0) {
+                m0 = m;
+                e0 = e;
+            }
+            n_ex += (int)tot;
         }
-        uint32_t tot;
-        const uint32_t pos = (uint32_t)n_ex + block_excl_scan<NT>(m != 0u ? 1u : 0u, s_red, &tot);
-        if (m != 0u) {
-            s_glist[pos] = gi;
-            s_gmask[pos] = m;
+        if (n_ex == 0) return;
+        const int64_t total = (int64_t)n_ex * len;
+        int64_t span = (total + geo.scan_blocks - 1) / geo.scan_blocks;
+        span = (span + 2 * kScanRowsPerIter - 1) / (2 * kScanRowsPerIter) * (2 * kScanRowsPerIter);
+        const int64_t pos0 = (int64_t)sbk * span;
+        if (pos0 >= total) return;
+        const int64_t end0 = pos0 + span < total ? pos0 + span : total;
+        const int e_lo = (int)(pos0 / len), e_hi = (int)((end0 - 1) / len);
+        // Pass 2: keep the exact groups of ranks e_lo .. e_hi.
+        if (NG <= NT && m0 != 0u && e0 >= e_lo && e0 <= e_hi && e0 - e_lo < kLocalGroups)
+            s_local[e0 - e_lo] = (uint32_t)tid * 256u + m0;
+        int rank0 = 0;
+        for (int g0 = 0; NG > NT && g0 < NG; g0 += NT) {
+            const int gi = g0 + tid;
+            const uint32_t m = gi < NG ? mask_of(gi) : 0u;
+            uint32_t tot;
+            const int e = rank0 + (int)block_excl_scan<NT>(m != 0u ? 1u : 0u, s_red, &tot);
+            if (m != 0u && e >= e_lo && e <= e_hi && e - e_lo < kLocalGroups)
+                s_local[e - e_lo] = (uint32_t)gi * 256u + m;
+            rank0 += (int)tot;
         }
-        n_ex += (int)tot;
-    }
-    __syncthreads();
-    if (n_ex == 0) return;
-
-    const int64_t len = a.len;
-    const int64_t total = (int64_t)n_ex * len;
-    int64_t span = (total + geo.scan_blocks - 1) / geo.scan_blocks;
-    span = (span + 2 * kScanRowsPerIter - 1) / (2 * kScanRowsPerIter) * (2 * kScanRowsPerIter);
-    int64_t pos = (int64_t)sbk * span;
-    const int64_t end = pos + span < total ? pos + span : total;
-    while (pos < end) {
-        const int e = (int)(pos / len);
-        const int64_t r0 = pos - (int64_t)e * len;
-        const int64_t r1 = (r0 + (end - pos) < len) ? r0 + (end - pos) : len;
-        const int gi = s_glist[e];
-        scan_segment<T, D, G>(a, w, gi / a.Hkv, gi % a.Hkv, s_gmask[e], r0, r1, s_hist);
-        pos += r1 - r0;
+        __syncthreads();
+        // A block's span is at most 512 rows when it is short, or about
+        // n_ex / scan_blocks + 1 of len rows, so it touches at most
+        // min(256 / len, 8) + 3 groups: s_local never fills.
+        do_span(n_ex, [&](int e, int &gi, uint32_t &m) {
+            const int at = e - e_lo < kLocalGroups ? e - e_lo : kLocalGroups - 1;
+            const uint32_t x = s_local[at];
+            gi = (int)(x >> 8);
+            m = x & 255u;
+        });
     }
 }
 
@@ -508,12 +545,11 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
 {
     using R = RowT<T, D>;
     constexpr int NT = kScoreThreads;
-    constexpr int kCands = kMaxCache / kSimSlots * kMaxR;   // merge candidates
+    const int kCands = ((a.M + kSimSlots - 1) / kSimSlots) * a.R;   // merge candidates
     __shared__ double s_red64[NT / 64];
     __shared__ uint32_t s_red32[NT / 64];
     __shared__ int32_t s_ret[kMaxR];
     __shared__ int32_t s_retcnt[kMaxR];
-    static_assert(20 * kCands <= ScoreLds<1>::kCand, "merge candidates fit the range block's LDS");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
     const int bh = cb / kCandRanges, s = cb % kCandRanges;
     const int M = a.M;
@@ -703,17 +739,16 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
 }
 
 // kSelect: the decode-step variant with range blocks (MODE_SELECT); otherwise
-// every head is exact and the grid holds scan blocks only.
+// every head is exact and the grid holds scan blocks only.  Dynamic LDS:
+// max(score_scan_lds(G), score_range_lds(merge candidates)) bytes.
 template <typename T, int D, int G, bool kSelect>
 __global__ __launch_bounds__(kScoreThreads, 4) void k_score(StepArgs a, Ws w, Geometry geo)
 {
-    __shared__ __attribute__((aligned(16))) unsigned char lds[ScoreLds<G>::kBytes];
-    // Range blocks (latency-bound) come first so they are dispatched before the
-    // bandwidth-bound scan blocks.
+    extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
     if (kSelect && (int)blockIdx.x < geo.cand_blocks)
         range_block<T, D>(a, w, (int)blockIdx.x, lds);
     else
-        scan_block<T, D, G>(a, w, geo, (int)blockIdx.x - (kSelect ? geo.cand_blocks : 0), lds);
+        scan_block<T, D, G, kSelect>(a, w, geo, (int)blockIdx.x - (kSelect ? geo.cand_blocks : 0), lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -733,14 +768,19 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
     const int f = blockIdx.x % geo.filter_blocks_per_head;
     if (a.mode == MODE_SELECT && w.path[bh] == PATH_REUSE) return;
 
+    // This block's scores and the head's histogram in one round trip.
+    const int64_t i0 = (int64_t)f * kFilterRows + (int64_t)tid * EPT;
+    const float4 *src = (const float4 *)(w.scores + (int64_t)bh * a.row_stride + i0);
+    const float4 v0 = src[0], v1 = src[1];
+    const uint32_t *hist = w.hist + (int64_t)bh * kHistBins;
+    uint32_t c[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[j] = hist[kHistBins - 1 - 4 * tid - j];
+
     // The bin b* that holds the kn-th largest score: the largest b with
     // count(bins >= b) >= kn.  Thread t holds bins 2047-4t .. 2044-4t.
     {
         const uint32_t kn = (uint32_t)(a.K < a.len ? a.K : a.len);
-        const uint32_t *hist = w.hist + (int64_t)bh * kHistBins;
-        uint32_t c[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) c[j] = hist[kHistBins - 1 - 4 * tid - j];
         uint32_t all;
         uint32_t above = block_excl_scan<NT>(c[0] + c[1] + c[2] + c[3], s_red, &all);
 #pragma unroll
@@ -751,9 +791,6 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
         __syncthreads();
     }
     const uint32_t kmin = s_bstar << kHistShift;
-    const int64_t i0 = (int64_t)f * kFilterRows + (int64_t)tid * EPT;
-    const float4 *src = (const float4 *)(w.scores + (int64_t)bh * a.row_stride + i0);
-    const float4 v0 = src[0], v1 = src[1];
     const float sv[EPT] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
     uint32_t keep = 0, n = 0;
 #pragma unroll
@@ -775,6 +812,9 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
 // k_final
 // ---------------------------------------------------------------------------
 
+constexpr int kTieMax = 64;        // bin sizes resolved by one wave
+constexpr int kSpecLoads = 4;      // speculative entry loads per thread
+
 template <int D, int NT>
 struct FinalSmem {
     uint64_t ent[kEntCache];        // the head's entries in index order, when they fit
@@ -786,8 +826,10 @@ struct FinalSmem {
     float qbar[D];
     double red64[NT / 64];
     uint32_t redu[NT / 64];
+    uint64_t tie[kTieMax];          // entries of the bin that holds the K-th largest
     unsigned long long rmax, rmin;
-    uint32_t found_digit, found_above, found_cnt;
+    uint64_t thr;
+    uint32_t found_digit, found_above, found_cnt, n_tie;
 };
 
 // Entries of one head, spread over regions of a fixed stride, read in order.
@@ -869,6 +911,77 @@ __device__ void radix_threshold(const Regions &rg, int K, FinalSmem<D, NT> &sm, 
     }
 }
 
+// Descending scan of sm.hist (nb <= 4 * NT bins): the bin where the count from
+// the top reaches k (found_digit), the count above it and its own count.
+template <int D, int NT>
+__device__ void find_bin(FinalSmem<D, NT> &sm, uint32_t nb, uint32_t k)
+{
+    const int tid = threadIdx.x;
+    uint32_t c[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int dgt = (int)nb - 1 - 4 * tid - j;
+        c[j] = dgt >= 0 ? sm.hist[dgt] : 0u;
+    }
+    uint32_t all;
+    uint32_t above = block_excl_scan<NT>(c[0] + c[1] + c[2] + c[3], sm.redu, &all);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (above < k && above + c[j] >= k) {
+            sm.found_digit = nb - 1u - 4u * tid - j;
+            sm.found_above = above;
+            sm.found_cnt = c[j];
+        }
+        above += c[j];
+    }
+    __syncthreads();
+}
+
+// Threshold rank of the Top-K over the n staged entries (n > K): the K-th largest
+// rank, so that the Top-K are exactly the entries e >= thr.  One histogram pass
+// over kHistBins bins that are linear in the score between the smallest and the
+// largest score (monotone in the score, so every entry of a higher bin outranks
+// every entry of a lower one); the K-th largest then lies in one bin, whose
+// entries one wave ranks exactly when there are at most kTieMax of them.  Returns
+// false when that bin is larger (heavy ties), leaving the radix select to decide.
+template <int D, int NT>
+__device__ bool value_threshold(const uint64_t *ent, int n, int K, FinalSmem<D, NT> &sm,
+                                uint64_t &thr)
+{
+    const int tid = threadIdx.x, lane = tid & 63;
+    const float smax = key_score(rank_key((uint64_t)sm.rmax));
+    const float smin = key_score(rank_key((uint64_t)sm.rmin));
+    const float range = smax - smin;
+    if (!(range > 0.0f) || !(range < 3.0e38f)) return false;   // block-uniform
+    const float scale = (float)(kHistBins - 1) / range;
+    for (int j = tid; j < n; j += NT) {
+        const float sc = key_score(rank_key(ent[j]));
+        const int bin = min((int)((sc - smin) * scale), kHistBins - 1);
+        atomicAdd(&sm.hist[bin], 1u);
+    }
+    __syncthreads();
+    find_bin<D, NT>(sm, kHistBins, (uint32_t)K);
+    const uint32_t bstar = sm.found_digit, cnt = sm.found_cnt;
+    const uint32_t k_rem = (uint32_t)K - sm.found_above;
+    if (cnt > (uint32_t)kTieMax) return false;
+    for (int j = tid; j < n; j += NT) {
+        const uint64_t e = ent[j];
+        const float sc = key_score(rank_key(e));
+        const int bin = min((int)((sc - smin) * scale), kHistBins - 1);
+        if ((uint32_t)bin == bstar) sm.tie[atomicAdd(&sm.n_tie, 1u)] = e;
+    }
+    __syncthreads();
+    if (tid < 64) {
+        const uint64_t e = lane < (int)cnt ? sm.tie[lane] : 0ull;
+        uint32_t above = 0;
+        for (int i = 0; i < (int)cnt; ++i) above += sm.tie[i] > e ? 1u : 0u;
+        if (lane < (int)cnt && above == k_rem - 1u) sm.thr = e;
+    }
+    __syncthreads();
+    thr = sm.thr;
+    return true;
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
 {
@@ -898,7 +1011,11 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
             for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = -1;
     }
 
-    // Path and the region counts of both layouts in one round trip.
+    // Path, the region counts of both layouts and the first entries of every
+    // region in one round trip (the entry loads are speculative: a region's
+    // count is known only afterwards).
+    const bool sel_mode = a.mode == MODE_SELECT;
+    const bool reuse = sel_mode && w.path[bh] == PATH_REUSE;
     const int nreg_s = (int)((a.len + kFilterRows - 1) / kFilterRows);
     const int rpt = (nreg_s + NT - 1) / NT;
     uint32_t scnt[kRegPerThread];
@@ -909,10 +1026,8 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
         const uint32_t x = w.surv_cnt[(int64_t)bh * a.n_regions + (ok ? r : 0)];
         scnt[u] = ok ? x : 0u;
     }
-    const bool sel_mode = a.mode == MODE_SELECT;
     const uint32_t ccnt_l = w.cand_cnt[(int64_t)bh * kCandRanges + (tid < kCandRanges ? tid : 0)];
     const uint32_t ccnt = (sel_mode && tid < kCandRanges) ? ccnt_l : 0u;
-    const bool reuse = sel_mode && w.path[bh] == PATH_REUSE;
 
     Regions rg;
     if (reuse) {
@@ -923,6 +1038,24 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
         rg.base = w.surv + (int64_t)bh * a.row_stride;
         rg.stride = kFilterRows;
         rg.nreg = nreg_s;
+    }
+    // spec slots per region: kSpecLoads * NT spread over the regions
+    int spec = (kSpecLoads * NT) / rg.nreg;
+    spec = spec < (int)rg.stride ? spec : (int)rg.stride;
+    uint64_t sv[kSpecLoads];
+#pragma unroll
+    for (int u = 0; u < kSpecLoads; ++u) {
+        const int e = tid + u * NT;
+        const int r = spec > 0 && e < spec * rg.nreg ? e / spec : 0;
+        const int j = spec > 0 && e < spec * rg.nreg ? e - r * spec : 0;
+        sv[u] = rg.base[(int64_t)r * rg.stride + j];
+    }
+    for (int i = tid; i < kHistBins; i += NT) sm.hist[i] = 0u;
+    if (tid == 0) {
+        sm.rmax = 0ull;
+        sm.rmin = ~0ull;
+        sm.n_tie = 0u;
+        sm.thr = 0ull;
     }
     {
         uint32_t mine = 0;
@@ -946,11 +1079,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
                 }
             }
         }
-        if (tid == 0) {
-            sm.pref[rg.nreg] = total;
-            sm.rmax = 0ull;
-            sm.rmin = ~0ull;
-        }
+        if (tid == 0) sm.pref[rg.nreg] = total;
         __syncthreads();
         rg.n = (int)total;
     }
@@ -958,23 +1087,59 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     rg.staged = nullptr;
     rg.top = rg.nreg > 1 ? 1 << (31 - __clz(rg.nreg - 1)) : 0;
     {
-        // Stage the entries (in index order) and find the largest and smallest rank.
+        // Stage the entries in index order (when they fit) and find the largest
+        // and smallest rank.
         uint64_t lmax = 0ull, lmin = ~0ull;
-        const bool stage = rg.n <= kEntCache;
-        for (int j0 = 0; j0 < rg.n; j0 += 4 * NT) {
-            uint64_t e[4];
+        if (rg.n <= kEntCache) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int j = j0 + u * NT + tid;
-                e[u] = rg.get(j < rg.n ? j : 0);
+            for (int u = 0; u < kSpecLoads; ++u) {
+                const int e = tid + u * NT;
+                if (spec > 0 && e < spec * rg.nreg) {
+                    const int r = e / spec, j = e - r * spec;
+                    const int at = (int)sm.pref[r] + j;
+                    if (at < (int)sm.pref[r + 1]) {
+                        sm.ent[at] = sv[u];
+                        lmax = sv[u] > lmax ? sv[u] : lmax;
+                        lmin = sv[u] < lmin ? sv[u] : lmin;
+                    }
+                }
             }
+            // entries past the speculative slots: one wave per region
+            for (int r = wave; r < rg.nreg; r += NW) {
+                const int p0 = (int)sm.pref[r], c = (int)sm.pref[r + 1] - p0;
+                for (int j0 = spec; j0 < c; j0 += 4 * 64) {
+                    uint64_t e[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int j = j0 + u * NT + tid;
-                if (j < rg.n) {
-                    if (stage) sm.ent[j] = e[u];
-                    lmax = e[u] > lmax ? e[u] : lmax;
-                    lmin = e[u] < lmin ? e[u] : lmin;
+                    for (int u = 0; u < 4; ++u) {
+                        const int j = j0 + u * 64 + lane;
+                        e[u] = rg.base[(int64_t)r * rg.stride + (j < c ? j : 0)];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int j = j0 + u * 64 + lane;
+                        if (j < c) {
+                            sm.ent[p0 + j] = e[u];
+                            lmax = e[u] > lmax ? e[u] : lmax;
+                            lmin = e[u] < lmin ? e[u] : lmin;
+                        }
+                    }
+                }
+            }
+        } else {
+            for (int j0 = 0; j0 < rg.n; j0 += 4 * NT) {
+                uint64_t e[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int j = j0 + u * NT + tid;
+                    e[u] = rg.get(j < rg.n ? j : 0);
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int j = j0 + u * NT + tid;
+                    if (j < rg.n) {
+                        lmax = e[u] > lmax ? e[u] : lmax;
+                        lmin = e[u] < lmin ? e[u] : lmin;
+                    }
                 }
             }
         }
@@ -990,24 +1155,32 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
             atomicMin(&sm.rmin, (unsigned long long)lmin);
         }
         __syncthreads();
-        if (stage) rg.staged = sm.ent;
+        if (rg.n <= kEntCache) rg.staged = sm.ent;
     }
 
-    // Top-K (Eq. 1 / Eq. 11), then the selected entries in index order.
-    uint64_t prefix, mask;
-    radix_threshold<D, NT>(rg, a.K, sm, prefix, mask);
+    // Top-K (Eq. 1 / Eq. 11): the entries e >= thr; then those in index order.
+    uint64_t thr = 0ull;
+    if (rg.n > a.K) {
+        bool done = false;
+        if (rg.staged) done = value_threshold<D, NT>(rg.staged, rg.n, a.K, sm, thr);
+        if (!done) {
+            uint64_t prefix, mask;
+            radix_threshold<D, NT>(rg, a.K, sm, prefix, mask);
+            thr = mask == 0ull ? 0ull : prefix;
+        }
+    }
     const int kn = rg.n < a.K ? rg.n : a.K;
     {
         const int ept = (rg.n + NT - 1) / NT;
         const int j0 = tid * ept < rg.n ? tid * ept : rg.n;
         const int j1 = j0 + ept < rg.n ? j0 + ept : rg.n;
         uint32_t mine = 0;
-        for (int j = j0; j < j1; ++j) mine += ((rg.get(j) & mask) >= prefix) ? 1u : 0u;
+        for (int j = j0; j < j1; ++j) mine += rg.get(j) >= thr ? 1u : 0u;
         uint32_t total;
         uint32_t pos = block_excl_scan<NT>(mine, sm.redu, &total);
         for (int j = j0; j < j1; ++j) {
             const uint64_t e = rg.get(j);
-            if ((e & mask) >= prefix && pos < (uint32_t)kMaxK)
+            if (e >= thr && pos < (uint32_t)kMaxK)
                 sm.sel[pos++] = ((uint64_t)rank_index(e) << 32) | rank_key(e);
         }
         __syncthreads();
@@ -1095,13 +1268,13 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
 // Launch on stream s; with a start/stop event pair the events are attached to the
 // dispatch itself, so they time exactly this kernel.
 template <typename F, typename... Args>
-static hipError_t launch(F kernel, dim3 grid, dim3 block, hipStream_t s, const Timing &tm,
-                         Args... args)
+static hipError_t launch(F kernel, dim3 grid, dim3 block, unsigned lds_bytes, hipStream_t s,
+                         const Timing &tm, Args... args)
 {
     if (tm.start != nullptr)
-        hipExtLaunchKernelGGL(kernel, grid, block, 0, s, tm.start, tm.stop, 0, args...);
+        hipExtLaunchKernelGGL(kernel, grid, block, lds_bytes, s, tm.start, tm.stop, 0, args...);
     else
-        hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+        hipLaunchKernelGGL(kernel, grid, block, lds_bytes, s, args...);
     return hipGetLastError();
 }
 
@@ -1115,7 +1288,7 @@ template <typename T, int D>
 static hipError_t sim_impl(const StepArgs &a, const Ws &w, hipStream_t s, const Timing &tm)
 {
     const int nsb = (a.M + kSimSlots - 1) / kSimSlots;
-    return launch(k_sim<T, D>, dim3((unsigned)(a.B * a.Hq * nsb)), dim3(kSimThreads), s, tm, a, w);
+    return launch(k_sim<T, D>, dim3((unsigned)(a.B * a.Hq * nsb)), dim3(kSimThreads), 0u, s, tm, a, w);
 }
 
 template <typename T, int D, int G>
@@ -1123,16 +1296,21 @@ static hipError_t score_impl(const StepArgs &a, const Ws &w, const Geometry &geo
                              const Timing &tm)
 {
     const int blocks = geo.scan_blocks + geo.cand_blocks;
-    if (a.mode == MODE_SELECT)
-        return launch(k_score<T, D, G, true>, dim3((unsigned)blocks), dim3(kScoreThreads), s, tm, a, w, geo);
-    return launch(k_score<T, D, G, false>, dim3((unsigned)blocks), dim3(kScoreThreads), s, tm, a, w, geo);
+    if (a.mode == MODE_SELECT) {
+        const int n_merge = ((a.M + kSimSlots - 1) / kSimSlots) * a.R;
+        const int r = score_range_lds(n_merge), c = score_scan_lds(G);
+        return launch(k_score<T, D, G, true>, dim3((unsigned)blocks), dim3(kScoreThreads),
+                      (unsigned)(r > c ? r : c), s, tm, a, w, geo);
+    }
+    return launch(k_score<T, D, G, false>, dim3((unsigned)blocks), dim3(kScoreThreads),
+                  (unsigned)score_scan_lds(G), s, tm, a, w, geo);
 }
 
 template <typename T, int D>
 static hipError_t final_impl(const StepArgs &a, const Ws &w, hipStream_t s, const Timing &tm)
 {
     return launch(k_final<T, D>, dim3((unsigned)(a.B * a.Hq * kFinalSlices)), dim3(kFinalThreads),
-                  s, tm, a, w);
+                  0u, s, tm, a, w);
 }
 
 template <typename T, int D>
@@ -1167,7 +1345,7 @@ hipError_t launch_filter(int dtype, const StepArgs &a, const Ws &w, const Geomet
 {
     (void)dtype;
     return launch(k_filter, dim3((unsigned)(a.B * a.Hq * geo.filter_blocks_per_head)),
-                  dim3(kScoreThreads), s, tm, a, w, geo);
+                  dim3(kScoreThreads), 0u, s, tm, a, w, geo);
 }
 hipError_t launch_final(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
                         hipStream_t s, const Timing &tm)
