@@ -287,11 +287,8 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
     const int bh = blockIdx.x / nsb, sb = blockIdx.x % nsb;
     const int n_valid = (int)(a.n_ins < (int64_t)M ? a.n_ins : (int64_t)M);
 
-    block_qbar<T, D, NT>((const T *)a.q + (int64_t)bh * a.q_head_stride, s_qbar, s_red);
-    if (sb == 0)
-        for (int t = tid; t < D; t += NT) w.qbar_cur[(int64_t)bh * D + t] = s_qbar[t];
-
-    // Eq. 6: 16 slots per wave, 4 lanes per cached row of D floats.
+    // Eq. 6: 16 slots per wave, 4 lanes per cached row of D floats.  The cached
+    // rows are loaded first, so that their latency overlaps the normalisation.
     const int local = wave * 16 + (lane >> 2);
     const int slot = sb * kSimSlots + local;
     const float4 *crow = (const float4 *)(w.qbar + ((int64_t)bh * M + (slot < n_valid ? slot : 0)) * D);
@@ -299,6 +296,11 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) c[s] = crow[s * 4 + p];   // clamped row: always in bounds
     const int scnt = w.cnt[(int64_t)bh * M + (slot < n_valid ? slot : 0)];
+
+    block_qbar<T, D, NT>((const T *)a.q + (int64_t)bh * a.q_head_stride, s_qbar, s_red);
+    if (sb == 0)
+        for (int t = tid; t < D; t += NT) w.qbar_cur[(int64_t)bh * D + t] = s_qbar[t];
+
     double acc = 0.0;
 #pragma unroll
     for (int s = 0; s < D / 16; ++s) {
@@ -369,8 +371,7 @@ __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint3
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
     const int bh0 = b * a.Hq + g * G;
     if (a.mode == MODE_SELECT && row0 == 0 && tid == 0) atomicAdd(&w.stats[STAT_SCANS], 1ull);
-    __syncthreads();   // the previous segment's histogram flush is done
-    for (int i = tid; i < G * kHistBins; i += kScoreThreads) s_hist[i] = 0u;
+    const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
     uint4 qv[G][R::kNV];
 #pragma unroll
     for (int j = 0; j < G; ++j) {
@@ -378,24 +379,24 @@ __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint3
 #pragma unroll
         for (int s = 0; s < R::kNV; ++s) qv[j][s] = qr[s * 4 + p];
     }
-    __syncthreads();
-    const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
-
-    for (int64_t base = row0; base < row1; base += 2 * kScanRowsPerIter) {
-        uint4 kv[2][R::kNV];
-        int64_t row[2];
+    // Two key rows per lane per iteration, loaded from clamped (in-bounds) rows.
+    uint4 kv[2][R::kNV];
+    int64_t row[2];
+    auto load = [&](int64_t base) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             row[u] = base + u * kScanRowsPerIter + wave * 16 + rl;
-            if (row[u] < row1) {
-                const uint4 *rp = (const uint4 *)(kbase + row[u] * D);
+            const uint4 *rp = (const uint4 *)(kbase + (row[u] < row1 ? row[u] : row0) * D);
 #pragma unroll
-                for (int s = 0; s < R::kNV; ++s) kv[u][s] = rp[s * 4 + p];
-            } else {
-#pragma unroll
-                for (int s = 0; s < R::kNV; ++s) kv[u][s] = make_uint4(0u, 0u, 0u, 0u);
-            }
+            for (int s = 0; s < R::kNV; ++s) kv[u][s] = rp[s * 4 + p];
         }
+    };
+    load(row0);   // the first rows are in flight while the histogram is cleared
+    __syncthreads();   // the previous segment's histogram flush is done
+    for (int i = tid; i < G * kHistBins; i += kScoreThreads) s_hist[i] = 0u;
+    __syncthreads();
+
+    for (int64_t base = row0; base < row1;) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             float acc[G];
@@ -421,6 +422,8 @@ __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint3
                 }
             }
         }
+        base += 2 * kScanRowsPerIter;
+        if (base < row1) load(base);
     }
     __syncthreads();
     for (int i = tid; i < G * kHistBins; i += kScoreThreads) {
@@ -488,6 +491,26 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
             }
             return m;
         };
+        if (NG <= 64) {
+            // One wave ranks the exact groups with a ballot; no block scans.
+            __shared__ int s_nex;
+            if (tid < 64) {
+                const uint32_t m = tid < NG ? mask_of(tid) : 0u;
+                const uint64_t bal = __ballot(m != 0u);
+                const int e = __popcll(bal & ((1ull << tid) - 1ull));
+                if (tid == 0) s_nex = __popcll(bal);
+                if (m != 0u) s_local[e] = (uint32_t)tid * 256u + m;
+            }
+            __syncthreads();
+            const int n_ex64 = s_nex;
+            if (n_ex64 == 0) return;
+            do_span(n_ex64, [&](int e, int &gi, uint32_t &m) {
+                const uint32_t x = s_local[e];
+                gi = (int)(x >> 8);
+                m = x & 255u;
+            });
+            return;
+        }
         // Pass 1: the number of exact groups, hence this block's rows (with at
         // most NT groups, one pass also ranks them).
         int n_ex = 0;
@@ -637,12 +660,29 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     if (s == 0 && a.dbg_ret)
         for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = i < nret ? s_ret[i] : -1;
 
-    // Eq. 8-9 restricted to this block's index range [lo, hi).
+    // Eq. 8-9 restricted to this block's index range [lo, hi).  The window (every
+    // one of its rows is a candidate) gets ranges of its own, about as many as its
+    // share of the candidates, so that no range block gathers far more rows than
+    // the others; the ranges stay in index order.
     const int64_t len = a.len;
-    const int64_t span = (len + kCandRanges - 1) / kCandRanges;
-    const int64_t lo = (int64_t)s * span;
-    const int64_t hi = lo + span < len ? lo + span : len;
     const int64_t w0 = len - a.W > 0 ? len - a.W : 0;
+    int n_win = 0;                                   // ranges covering [w0, len)
+    if (a.W > 0) {
+        const int64_t share = (80ll * a.W + 10ll * a.W + 3ll * a.R * a.K - 1) / (10ll * a.W + 3ll * a.R * a.K);
+        n_win = w0 == 0 ? kCandRanges : (int)(share < 1 ? 1 : (share > kCandRanges - 1 ? kCandRanges - 1 : share));
+    }
+    const int n_old = kCandRanges - n_win;           // ranges covering [0, w0)
+    int64_t lo, hi;
+    if (s < n_old) {
+        const int64_t span = (w0 + n_old - 1) / n_old;
+        lo = (int64_t)s * span;
+        hi = lo + span < w0 ? lo + span : w0;
+    } else {
+        const int64_t span = (len - w0 + n_win - 1) / n_win;
+        lo = w0 + (int64_t)(s - n_old) * span;
+        hi = lo + span < len ? lo + span : len;
+    }
+    if (lo > hi) lo = hi;
     uint32_t *bitmap = (uint32_t *)lds;                    // reuses the merge space
     int32_t *list = (int32_t *)(lds + kSegWords * 4);
     uint64_t *ents = w.cand_ent + ((int64_t)bh * kCandRanges + s) * a.cand_cap;
