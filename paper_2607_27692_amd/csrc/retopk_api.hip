@@ -4,6 +4,8 @@
 #include "retopk.h"
 #include "retopk_internal.h"
 
+#include <hip/hip_ext.h>
+
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -131,9 +133,9 @@ Geometry make_geometry(const retopk_handle_s *h, int64_t len, int mode)
 }
 
 // Event pair for the next launch of kernel `kid` when profiling is on.
-retopk_status timing_for(retopk_handle h, int kid, Timing *tm)
+retopk_status timing_for(retopk_handle h, int kid, hipEvent_t *start, hipEvent_t *stop)
 {
-    *tm = Timing{};
+    *start = *stop = nullptr;
     if (!h->prof) return RETOPK_OK;
     if (h->ev_used / 2 >= (size_t)kProfileMaxLaunches) {
         h->prof_overflow = true;
@@ -144,8 +146,8 @@ retopk_status timing_for(retopk_handle h, int kid, Timing *tm)
         if (hipEventCreate(&e) != hipSuccess) return RETOPK_ERR_HIP;
         h->ev.push_back(e);
     }
-    tm->start = h->ev[h->ev_used];
-    tm->stop = h->ev[h->ev_used + 1];
+    *start = h->ev[h->ev_used];
+    *stop = h->ev[h->ev_used + 1];
     h->ev_kernel.push_back(kid);
     h->ev_used += 2;
     return RETOPK_OK;
@@ -157,23 +159,39 @@ retopk_status fail(retopk_handle h)
     return RETOPK_ERR_HIP;
 }
 
-// Launches one step (or one prefill query) in `mode`.
+// Launches one step (or one prefill query) in `mode`: SELECT runs k_sim, k_score,
+// k_filter, k_final; the other modes k_score (scan only), k_filter, k_final.
+// With profiling on, events are attached to each kernel's dispatch.
 retopk_status run_step(retopk_handle h, const StepArgs &a, int mode, hipStream_t s)
 {
     const Geometry geo = make_geometry(h, a.len, mode);
     const int dt = h->cfg.dtype;
-    Timing tm;
-    retopk_status st;
-    if (mode == MODE_SELECT) {
-        if ((st = timing_for(h, KID_SIM, &tm)) != RETOPK_OK) return st;
-        if (launch_sim(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
+    int kinds[4], n = 0;
+    if (mode == MODE_SELECT) kinds[n++] = KERNEL_SIM;
+    kinds[n++] = KERNEL_SCORE;
+    kinds[n++] = KERNEL_FILTER;
+    kinds[n++] = KERNEL_FINAL;
+    KernelDesc d[4];
+    for (int i = 0; i < n; ++i) describe_kernel(kinds[i], dt, a, geo, &d[i]);
+    StepArgs av = a;
+    Ws wv = h->w;
+    Geometry gv = geo;
+    void *args[3] = {&av, &wv, &gv};
+
+    for (int i = 0; i < n; ++i) {
+        int kid = KID_FINAL;
+        if (kinds[i] == KERNEL_SIM) kid = KID_SIM;
+        else if (kinds[i] == KERNEL_SCORE) kid = mode == MODE_SELECT ? KID_SCORE : KID_SCAN;
+        else if (kinds[i] == KERNEL_FILTER) kid = KID_FILTER;
+        hipEvent_t start, stop;
+        retopk_status st = timing_for(h, kid, &start, &stop);
+        if (st != RETOPK_OK) return st;
+        hipError_t e = start
+            ? hipExtLaunchKernel(d[i].func, d[i].grid, d[i].block, args, d[i].lds_bytes, s, start,
+                                 stop, 0)
+            : hipLaunchKernel(d[i].func, d[i].grid, d[i].block, args, d[i].lds_bytes, s);
+        if (e != hipSuccess) return fail(h);
     }
-    if ((st = timing_for(h, mode == MODE_SELECT ? KID_SCORE : KID_SCAN, &tm)) != RETOPK_OK) return st;
-    if (launch_score(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
-    if ((st = timing_for(h, KID_FILTER, &tm)) != RETOPK_OK) return st;
-    if (launch_filter(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
-    if ((st = timing_for(h, KID_FINAL, &tm)) != RETOPK_OK) return st;
-    if (launch_final(dt, a, h->w, geo, s, tm) != hipSuccess) return fail(h);
     return RETOPK_OK;
 }
 

@@ -110,21 +110,21 @@ struct Geometry {
     int filter_blocks_per_head;
 };
 
-// Optional start/stop events attached to one kernel dispatch (both null: none).
-struct Timing {
-    hipEvent_t start = nullptr;
-    hipEvent_t stop = nullptr;
+// One kernel of a step, ready to launch (hipLaunchKernel) or to put in a graph
+// node: the kernel takes (StepArgs, Ws) when nargs == 2 and (StepArgs, Ws,
+// Geometry) when nargs == 3, all by value.
+struct KernelDesc {
+    const void *func;
+    dim3 grid;
+    dim3 block;
+    unsigned lds_bytes;      // dynamic LDS
+    int nargs;
 };
+enum : int { KERNEL_SIM = 0, KERNEL_SCORE = 1, KERNEL_FILTER = 2, KERNEL_FINAL = 3 };
 
-// Launchers (retopk_kernels.hip).  dtype: 0 = f32, 1 = bf16.
-hipError_t launch_sim(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                      hipStream_t s, const Timing &tm);
-hipError_t launch_score(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                        hipStream_t s, const Timing &tm);
-hipError_t launch_filter(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                         hipStream_t s, const Timing &tm);
-hipError_t launch_final(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                        hipStream_t s, const Timing &tm);
+// Fills *k for kernel `which` of a step in a.mode (retopk_kernels.hip).
+// dtype: 0 = f32, 1 = bf16.
+void describe_kernel(int which, int dtype, const StepArgs &a, const Geometry &geo, KernelDesc *k);
 bool shape_supported(int dtype, int d, int g);
 
 }  // namespace retopk

@@ -1305,19 +1305,6 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
 // Launchers
 // ---------------------------------------------------------------------------
 
-// Launch on stream s; with a start/stop event pair the events are attached to the
-// dispatch itself, so they time exactly this kernel.
-template <typename F, typename... Args>
-static hipError_t launch(F kernel, dim3 grid, dim3 block, unsigned lds_bytes, hipStream_t s,
-                         const Timing &tm, Args... args)
-{
-    if (tm.start != nullptr)
-        hipExtLaunchKernelGGL(kernel, grid, block, lds_bytes, s, tm.start, tm.stop, 0, args...);
-    else
-        hipLaunchKernelGGL(kernel, grid, block, lds_bytes, s, args...);
-    return hipGetLastError();
-}
-
 bool shape_supported(int dtype, int d, int g)
 {
     return (dtype == 0 || dtype == 1) && (d == 64 || d == 128) &&
@@ -1325,75 +1312,63 @@ bool shape_supported(int dtype, int d, int g)
 }
 
 template <typename T, int D>
-static hipError_t sim_impl(const StepArgs &a, const Ws &w, hipStream_t s, const Timing &tm)
+static void sim_desc(const StepArgs &a, KernelDesc *k)
 {
     const int nsb = (a.M + kSimSlots - 1) / kSimSlots;
-    return launch(k_sim<T, D>, dim3((unsigned)(a.B * a.Hq * nsb)), dim3(kSimThreads), 0u, s, tm, a, w);
+    *k = KernelDesc{(const void *)&k_sim<T, D>, dim3((unsigned)(a.B * a.Hq * nsb)), dim3(kSimThreads), 0u, 2};
 }
 
 template <typename T, int D, int G>
-static hipError_t score_impl(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s,
-                             const Timing &tm)
+static void score_desc(const StepArgs &a, const Geometry &geo, KernelDesc *k)
 {
-    const int blocks = geo.scan_blocks + geo.cand_blocks;
+    const unsigned blocks = (unsigned)(geo.scan_blocks + geo.cand_blocks);
     if (a.mode == MODE_SELECT) {
         const int n_merge = ((a.M + kSimSlots - 1) / kSimSlots) * a.R;
         const int r = score_range_lds(n_merge), c = score_scan_lds(G);
-        return launch(k_score<T, D, G, true>, dim3((unsigned)blocks), dim3(kScoreThreads),
-                      (unsigned)(r > c ? r : c), s, tm, a, w, geo);
+        *k = KernelDesc{(const void *)&k_score<T, D, G, true>, dim3(blocks), dim3(kScoreThreads),
+                        (unsigned)(r > c ? r : c), 3};
+    } else {
+        *k = KernelDesc{(const void *)&k_score<T, D, G, false>, dim3(blocks), dim3(kScoreThreads),
+                        (unsigned)score_scan_lds(G), 3};
     }
-    return launch(k_score<T, D, G, false>, dim3((unsigned)blocks), dim3(kScoreThreads),
-                  (unsigned)score_scan_lds(G), s, tm, a, w, geo);
 }
 
 template <typename T, int D>
-static hipError_t final_impl(const StepArgs &a, const Ws &w, hipStream_t s, const Timing &tm)
+static void final_desc(const StepArgs &a, KernelDesc *k)
 {
-    return launch(k_final<T, D>, dim3((unsigned)(a.B * a.Hq * kFinalSlices)), dim3(kFinalThreads),
-                  0u, s, tm, a, w);
+    *k = KernelDesc{(const void *)&k_final<T, D>, dim3((unsigned)(a.B * a.Hq * kFinalSlices)),
+                    dim3(kFinalThreads), 0u, 2};
 }
 
 template <typename T, int D>
-static hipError_t score_g(const StepArgs &a, const Ws &w, const Geometry &geo, hipStream_t s,
-                          const Timing &tm)
+static void score_g(const StepArgs &a, const Geometry &geo, KernelDesc *k)
 {
     switch (a.G) {
-    case 1: return score_impl<T, D, 1>(a, w, geo, s, tm);
-    case 2: return score_impl<T, D, 2>(a, w, geo, s, tm);
-    case 4: return score_impl<T, D, 4>(a, w, geo, s, tm);
-    default: return score_impl<T, D, 8>(a, w, geo, s, tm);
+    case 1: return score_desc<T, D, 1>(a, geo, k);
+    case 2: return score_desc<T, D, 2>(a, geo, k);
+    case 4: return score_desc<T, D, 4>(a, geo, k);
+    default: return score_desc<T, D, 8>(a, geo, k);
     }
 }
 
-hipError_t launch_sim(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                      hipStream_t s, const Timing &tm)
+void describe_kernel(int which, int dtype, const StepArgs &a, const Geometry &geo, KernelDesc *k)
 {
-    (void)geo;
-    if (dtype == 1)
-        return a.D == 64 ? sim_impl<uint16_t, 64>(a, w, s, tm) : sim_impl<uint16_t, 128>(a, w, s, tm);
-    return a.D == 64 ? sim_impl<float, 64>(a, w, s, tm) : sim_impl<float, 128>(a, w, s, tm);
-}
-hipError_t launch_score(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                        hipStream_t s, const Timing &tm)
-{
-    if (dtype == 1)
-        return a.D == 64 ? score_g<uint16_t, 64>(a, w, geo, s, tm) : score_g<uint16_t, 128>(a, w, geo, s, tm);
-    return a.D == 64 ? score_g<float, 64>(a, w, geo, s, tm) : score_g<float, 128>(a, w, geo, s, tm);
-}
-hipError_t launch_filter(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                         hipStream_t s, const Timing &tm)
-{
-    (void)dtype;
-    return launch(k_filter, dim3((unsigned)(a.B * a.Hq * geo.filter_blocks_per_head)),
-                  dim3(kScoreThreads), 0u, s, tm, a, w, geo);
-}
-hipError_t launch_final(int dtype, const StepArgs &a, const Ws &w, const Geometry &geo,
-                        hipStream_t s, const Timing &tm)
-{
-    (void)geo;
-    if (dtype == 1)
-        return a.D == 64 ? final_impl<uint16_t, 64>(a, w, s, tm) : final_impl<uint16_t, 128>(a, w, s, tm);
-    return a.D == 64 ? final_impl<float, 64>(a, w, s, tm) : final_impl<float, 128>(a, w, s, tm);
+    const bool bf = dtype == 1, d64 = a.D == 64;
+    switch (which) {
+    case KERNEL_SIM:
+        if (bf) return d64 ? sim_desc<uint16_t, 64>(a, k) : sim_desc<uint16_t, 128>(a, k);
+        return d64 ? sim_desc<float, 64>(a, k) : sim_desc<float, 128>(a, k);
+    case KERNEL_SCORE:
+        if (bf) return d64 ? score_g<uint16_t, 64>(a, geo, k) : score_g<uint16_t, 128>(a, geo, k);
+        return d64 ? score_g<float, 64>(a, geo, k) : score_g<float, 128>(a, geo, k);
+    case KERNEL_FILTER:
+        *k = KernelDesc{(const void *)&k_filter, dim3((unsigned)(a.B * a.Hq * geo.filter_blocks_per_head)),
+                        dim3(kScoreThreads), 0u, 3};
+        return;
+    default:
+        if (bf) return d64 ? final_desc<uint16_t, 64>(a, k) : final_desc<uint16_t, 128>(a, k);
+        return d64 ? final_desc<float, 64>(a, k) : final_desc<float, 128>(a, k);
+    }
 }
 
 }  // namespace retopk

@@ -222,3 +222,4 @@ def test_determinism_16k():
     for key in ("qbar", "supp", "cnt"):
         assert np.array_equal(a[0][key], b[0][key])
     assert a[4] == b[4]
+
