@@ -351,12 +351,12 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
 // ---------------------------------------------------------------------------
 
 // Dynamic LDS of k_score (bytes): the scan blocks' histograms, or a range
-// block's Top-R merge candidates (20 bytes each), which later hold the union
+// block's Top-R merge candidates (24 bytes each), which later hold the union
 // bitmap segment and the candidate list.
 __host__ __device__ constexpr int score_scan_lds(int g) { return g * kHistBins * 4; }
 __host__ __device__ constexpr int score_range_lds(int n_merge)
 {
-    return 20 * n_merge > kSegWords * 4 + kCandList * 4 ? 20 * n_merge : kSegWords * 4 + kCandList * 4;
+    return 24 * n_merge > kSegWords * 4 + kCandList * 4 ? 24 * n_merge : kSegWords * 4 + kCandList * 4;
 }
 constexpr int kLocalGroups = 512;   // exact KV groups one scan block's rows can touch
 
@@ -569,10 +569,10 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     using R = RowT<T, D>;
     constexpr int NT = kScoreThreads;
     const int kCands = ((a.M + kSimSlots - 1) / kSimSlots) * a.R;   // merge candidates
-    __shared__ double s_red64[NT / 64];
     __shared__ uint32_t s_red32[NT / 64];
     __shared__ int32_t s_ret[kMaxR];
     __shared__ int32_t s_retcnt[kMaxR];
+    __shared__ double s_mx;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
     const int bh = cb / kCandRanges, s = cb % kCandRanges;
     const int M = a.M;
@@ -582,14 +582,15 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     double *c_rho = (double *)lds;
     int32_t *c_slot = (int32_t *)(lds + 8 * kCands);
     int32_t *c_cnt = (int32_t *)(lds + 12 * kCands);
-    int32_t *c_rank = (int32_t *)(lds + 16 * kCands);
+    int32_t *c_age = (int32_t *)(lds + 16 * kCands);
+    int32_t *c_rank = (int32_t *)(lds + 20 * kCands);
     const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
 
-    // Independent loads first: k_sim block maxima, the blocks' Top-R lists, q.
-    const double bmax_l = w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + (tid < nsb ? tid : 0)];
-    const double bmax = tid < nsb ? bmax_l : -INFINITY;
+    // Independent loads first: the k_sim blocks' Top-R lists (each one sorted,
+    // most similar first, invalid entries last) and q.
     const int per = a.R;                        // list length of a full k_sim block
     const int nc = nsb * per;
+    const int age0 = (int)((a.n_ins - 1) % M);
     for (int c = tid; c < nc; c += NT) {
         const int sb = c / per, j = c - sb * per;
         const int nloc = n_valid - sb * kSimSlots;
@@ -601,18 +602,63 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
         c_slot[c] = valid ? sl : -1;
         c_rho[c] = valid ? rr : -INFINITY;
         c_cnt[c] = valid ? cn : 0;
+        c_age[c] = valid ? slot_age(age0, sl, M) : 0x7FFFFFFF;
         c_rank[c] = 0;
     }
+    if (tid == 0) s_mx = -INFINITY;
     uint4 qv[R::kNV];
     {
         const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)bh * a.q_head_stride);
 #pragma unroll
         for (int v = 0; v < R::kNV; ++v) qv[v] = qr[v * 4 + p];
     }
+    __syncthreads();
 
-    // rho_max (Eq. 7) and the path (Eq. 13).  block_reduce's barriers also publish
-    // the merge candidates.
-    const double mx = block_reduce<NT>(bmax, s_red64, [](double x, double y) { return fmax(x, y); });
+    // Eq. 7: merge the blocks' Top-R lists.  The global rank of candidate c is
+    // its position in its own list plus, for every other list, the number of
+    // entries that are more similar, or equally similar and newer; one thread
+    // counts one (candidate, list) pair.  The rank-0 candidate gives rho_max.
+    for (int pr = tid; pr < nc * nsb; pr += NT) {
+        const int c = pr / nsb, o = pr - c * nsb;
+        const int32_t sl = c_slot[c];
+        if (sl < 0 || o == c / per) continue;
+        const double rc = c_rho[c];
+        const int ac = c_age[c];
+        // Invalid entries carry rho = -inf and never count.  All reads of a
+        // chunk are issued before any comparison.
+        int cnt = 0;
+        for (int k0 = 0; k0 < per; k0 += 4) {
+            double rr[4];
+            int aa[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int e = o * per + (k0 + u < per ? k0 + u : per - 1);
+                rr[u] = c_rho[e];
+                aa[u] = c_age[e];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool beats = (rr[u] > rc) | ((rr[u] == rc) & (aa[u] < ac));
+                cnt += (beats & (k0 + u < per)) ? 1 : 0;
+            }
+        }
+        if (cnt) atomicAdd(&c_rank[c], cnt);
+    }
+    __syncthreads();
+    for (int c = tid; c < nc; c += NT) {
+        const int32_t sl = c_slot[c];
+        if (sl < 0) continue;
+        const int rank = c - (c / per) * per + c_rank[c];
+        if (rank < nret_all) {
+            s_ret[rank] = sl;
+            s_retcnt[rank] = c_cnt[c];
+        }
+        if (rank == 0) s_mx = c_rho[c];
+    }
+    __syncthreads();
+
+    // rho_max and the path (Eq. 13).
+    const double mx = s_mx;
     const int8_t path = mx < (double)a.tau ? PATH_FALLBACK : PATH_REUSE;
     const int nret = path == PATH_REUSE ? nret_all : 0;
     if (s == 0 && tid == 0) {
@@ -626,37 +672,6 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
             for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = -1;
         return;
     }
-
-    // Eq. 7: merge the blocks' Top-R lists.  Candidate c is the rank-th retrieved
-    // entry, rank = number of candidates that are more similar, or equally
-    // similar and newer; P threads share the comparisons of one candidate.
-    {
-        const int age0 = (int)((a.n_ins - 1) % M);
-        int P = 1;
-        while (P * 2 <= 64 && P * 2 * nc <= NT) P *= 2;
-        for (int pair = tid; pair < nc * P; pair += NT) {
-            const int c = pair / P, sub = pair - c * P;
-            const int32_t sl = c_slot[c];
-            if (sl < 0) continue;
-            const double rc = c_rho[c];
-            const int ac = slot_age(age0, sl, M);
-            int cnt = 0;
-            for (int o = sub; o < nc; o += P) {
-                const int32_t so = c_slot[o];
-                cnt += (so >= 0 && better(c_rho[o], slot_age(age0, so, M), rc, ac)) ? 1 : 0;
-            }
-            atomicAdd(&c_rank[c], cnt);
-        }
-    }
-    __syncthreads();
-    for (int c = tid; c < nc; c += NT) {
-        const int rank = c_rank[c];
-        if (c_slot[c] >= 0 && rank < nret) {
-            s_ret[rank] = c_slot[c];
-            s_retcnt[rank] = c_cnt[c];
-        }
-    }
-    __syncthreads();
     if (s == 0 && a.dbg_ret)
         for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = i < nret ? s_ret[i] : -1;
 
@@ -748,21 +763,22 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
             }
             __syncthreads();
             const int nr = (int)(seg_total - rb < (uint32_t)kCandList ? seg_total - rb : kCandList);
-            // Eq. 10 on this round: 4 lanes per key row, two rows per lane in flight.
-            for (int base = 0; base < nr; base += 2 * kScanRowsPerIter) {
-                uint4 kv[2][R::kNV];
-                int ci[2], cidx[2];
+            // Eq. 10 on this round: 4 lanes per key row, four rows per lane in
+            // flight, loaded from clamped (in-bounds) list positions.
+            constexpr int GU = 4;
+            for (int base = 0; base < nr; base += GU * kScanRowsPerIter) {
+                uint4 kv[GU][R::kNV];
+                int ci[GU], cidx[GU];
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
+                for (int u = 0; u < GU; ++u) {
                     ci[u] = base + u * kScanRowsPerIter + wave * 16 + rl;
-                    cidx[u] = ci[u] < nr ? list[ci[u]] : 0;
+                    cidx[u] = list[ci[u] < nr ? ci[u] : nr - 1];
                     const uint4 *rp = (const uint4 *)(kbase + (int64_t)cidx[u] * D);
 #pragma unroll
-                    for (int v = 0; v < R::kNV; ++v)
-                        kv[u][v] = ci[u] < nr ? rp[v * 4 + p] : make_uint4(0u, 0u, 0u, 0u);
+                    for (int v = 0; v < R::kNV; ++v) kv[u][v] = rp[v * 4 + p];
                 }
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
+                for (int u = 0; u < GU; ++u) {
                     float s0 = 0.0f;
 #pragma unroll
                     for (int v = 0; v < R::kNV; ++v) s0 = Dot<T>::f(kv[u][v], qv[v], s0);
