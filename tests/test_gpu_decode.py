@@ -140,19 +140,27 @@ def test_decode_lockstep_16k_two_groups():
     assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * w.steps
 
 
-@pytest.mark.parametrize("name", ["32k", "128k"])
+@pytest.mark.parametrize("name", ["32k", "128k", "stress"])
 def test_decode_full_size_sampled(name):
     """Full-size layer shapes: the cache starts from the prompt-tail queries with
-    seeded supports (no prefill), and 3 steps run in lock-step; KV groups 0 and
-    Hkv-1 are compared."""
+    seeded supports (no prefill), and 3 steps run in lock-step; KV group 0 of the
+    first sequence and the last KV group of the last sequence are compared (the
+    stress workload has 4 sequences, K = 1024 and tau = 0.9)."""
     w = WORKLOADS[name]
     print(f"decode full-size {w.name}", flush=True)
     inp = make_inputs(w)
     p = params_of(w)
-    supp, cnt = make_support_state(inp)
-    qbar = np.stack([np.stack([O.normalize(inp.q_tail[b, h, u]) for u in range(w.cache_cap)])
-                     for b in range(w.batch) for h in range(w.n_q_heads)])
-    heads = list(range(0, w.group)) + list(range(w.n_q_heads - w.group, w.n_q_heads))
+    BH = w.batch * w.n_q_heads
+    heads = list(range(0, w.group)) + list(range(BH - w.group, BH))
+    # every head gets a cache state, except in the 4-sequence workload, where the
+    # heads that are not compared keep an empty cache state (zero queries: they
+    # take the fallback path, so every KV group is scanned there)
+    drawn = heads if w.batch > 1 else list(range(BH))
+    supp, cnt = make_support_state(inp, heads=drawn)
+    qbar = np.zeros((BH, w.cache_cap, w.head_dim), np.float32)
+    for bh in drawn:
+        b, h = divmod(bh, w.n_q_heads)
+        qbar[bh] = np.stack([O.normalize(inp.q_tail[b, h, u]) for u in range(w.cache_cap)])
     tally, paths = _lockstep(w, inp, p, heads, 3,
                              state0=(qbar, supp, cnt, w.cache_cap, 1))
     print(tally, paths.tolist(), flush=True)
@@ -223,3 +231,33 @@ def test_determinism_16k():
         assert np.array_equal(a[0][key], b[0][key])
     assert a[4] == b[4]
 
+
+
+VARIANTS = [
+    ("r1", dict(r=1)),                 # a single retrieved entry
+    ("c1", dict(cache_cap=1)),         # a one-entry cache
+    ("tau_minus1", dict(tau=-1.0)),    # never falls back
+    ("no_refresh", dict(refresh=0)),   # refresh off
+    ("no_window", dict(window=0)),     # supports only; fewer than K candidates occur
+    ("always_fallback", dict(tau=2.0)),
+]
+
+
+@pytest.mark.parametrize("label, change", VARIANTS, ids=[v[0] for v in VARIANTS])
+def test_decode_lockstep_variants(label, change):
+    """The ablation settings of the paper's component study (single retrieved
+    entry, one-entry cache, no fallback, no refresh, no recent window) and the
+    all-fallback limit, on the fp32 single-head workload, all steps in lock-step."""
+    w = WORKLOADS["tiny"].with_(**change)
+    print(f"decode lock-step {w.name} {label}", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w)
+    tally, paths = _lockstep(w, inp, p, [0], w.steps)
+    print(tally, flush=True)
+    assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == w.steps
+    if label == "tau_minus1":
+        assert (paths == O.FALLBACK).sum() == 0
+    if label == "no_refresh":
+        assert (paths == O.REFRESH).sum() == 0
+    if label == "always_fallback":
+        assert ((paths == O.FALLBACK) | (paths == O.REFRESH)).all()
