@@ -23,7 +23,7 @@ class OrcConfig(C.Structure):
         ("batch", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
         ("head_dim", C.c_int32), ("max_len", C.c_int64), ("k", C.c_int32),
         ("cache_cap", C.c_int32), ("r", C.c_int32), ("window", C.c_int32),
-        ("tau", C.c_float), ("refresh", C.c_int32),
+        ("tau", C.c_float), ("refresh", C.c_int32), ("retrieval", C.c_int32),
     ]
 
 
@@ -96,11 +96,12 @@ class Params:
     window: int
     tau: float
     refresh: int
+    retrieval: int = 0     # 0: the R most similar entries (Eq. 7); 1: the R most recent
 
     def cstruct(self) -> OrcConfig:
         return OrcConfig(self.batch, self.n_q_heads, self.n_kv_heads, self.head_dim,
                          self.max_len, self.k, self.cache_cap, self.r, self.window,
-                         self.tau, self.refresh)
+                         self.tau, self.refresh, self.retrieval)
 
     @property
     def cand_cap(self) -> int:

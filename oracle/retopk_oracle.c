@@ -181,6 +181,7 @@ static int config_ok(const orc_config *c)
     if (c->max_len < 1 || c->max_len > INT32_MAX) return 0;
     if (c->k < 1 || c->cache_cap < 0 || c->r < 1 || c->window < 0 || c->refresh < 0) return 0;
     if (!isfinite(c->tau)) return 0;
+    if (c->retrieval != 0 && c->retrieval != 1) return 0;
     return 1;
 }
 
@@ -322,7 +323,10 @@ int orc_decode_step(orc_handle *h, const float *q, const float *k, const float *
             } else if (refresh) {
                 path = ORC_REFRESH;
             } else {
-                /* Eq. 6: cosine similarity to every cached query. */
+                /* Eq. 6: cosine similarity to every cached query.  rho_max is
+                 * the largest similarity among the entries retrieval will use:
+                 * all of them for Eq. 7 (its best one is retrieved), the R most
+                 * recent ones for recent-R retrieval. */
                 rho_max = -INFINITY;
                 for (int64_t s = 0; s < n_valid; ++s) {
                     const float *cq = h->qbar + (head * C + s) * d;
@@ -330,7 +334,9 @@ int orc_decode_step(orc_handle *h, const float *q, const float *k, const float *
                     for (int j = 0; j < d; ++j)
                         acc += (double)qbar[j] * (double)cq[j];
                     rho[s] = acc;
-                    if (acc > rho_max) rho_max = acc;
+                    const int64_t age = ((h->n_ins - 1 - s) % C + C) % C;
+                    const int counted = c->retrieval == 0 || age < R;
+                    if (counted && acc > rho_max) rho_max = acc;
                 }
                 /* Eq. 13 second case, Sec. 3.4: fall back when rho_max < tau. */
                 path = rho_max < (double)c->tau ? ORC_FALLBACK : ORC_REUSE;
@@ -350,7 +356,9 @@ int orc_decode_step(orc_handle *h, const float *q, const float *k, const float *
                         int32_t x = slot_order[s], y = slot_order[best];
                         int64_t age_x = ((h->n_ins - 1 - x) % C + C) % C;
                         int64_t age_y = ((h->n_ins - 1 - y) % C + C) % C;
-                        if (rho[x] > rho[y] || (rho[x] == rho[y] && age_x < age_y))
+                        const int newer = age_x < age_y;
+                        if (c->retrieval == 0 ? (rho[x] > rho[y] || (rho[x] == rho[y] && newer))
+                                              : newer)
                             best = s;
                     }
                     int32_t tmp = slot_order[a];

@@ -42,6 +42,9 @@ typedef struct {
     int32_t window;       /* W: recent window                             */
     float   tau;          /* similarity fallback threshold                */
     int32_t refresh;      /* T_r in the paper: refresh period, 0 = off    */
+    int32_t retrieval;    /* 0: the R most similar entries (Eq. 7); 1: the R
+                             most recently inserted ones, the recent-R
+                             alternative of the component ablation (Table 3) */
 } orc_config;
 
 /* Path codes, one per (b, query head) and step. */

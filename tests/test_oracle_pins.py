@@ -503,3 +503,51 @@ def test_attend_on_given_set_matches_exact(oracle_lib, golden):
         idx = np.array([i for i in case["sel"] if i >= 0], np.int32)
         want = np.array([_closed(s) for s in case["out"]])
         np.testing.assert_allclose(O.attend(q, k, v, idx[::-1].copy()), want, rtol=2e-7, atol=1e-7)
+
+
+def test_recent_r_retrieval(oracle_lib, tiny):
+    """Recent-R retrieval (the component ablation, Table 3): on every reuse step the
+    retrieved entries are the R most recent insertions, newest first; rho_max is
+    the best similarity among them and decides the fallback (Eq. 13); candidates
+    are the union of their supports and the window (Eq. 8-9)."""
+    w = tiny.w
+    p = _workload_params(w, retrieval=1)
+    seen = {"reuse": 0, "fallback": 0}
+
+    def check(t, before, out, sel, info):
+        L = w.step_len(t)
+        path = int(info.path[0])
+        if path not in (O.REUSE, O.FALLBACK):
+            return
+        nv = min(before["n_inserted"], w.cache_cap)
+        recent = [(before["n_inserted"] - 1 - i) % w.cache_cap for i in range(min(w.r, nv))]
+        q = tiny.q_dec[t][0, 0].astype(np.float64)
+        qb = q / np.linalg.norm(q)
+        rho = before["qbar"][0, :nv].astype(np.float64) @ qb
+        assert abs(info.rho_max[0] - rho[recent].max()) < 1e-6
+        assert (path == O.FALLBACK) == (info.rho_max[0] < w.tau)
+        if path == O.FALLBACK:
+            seen["fallback"] += 1
+            return
+        seen["reuse"] += 1
+        assert info.retrieved[0, :len(recent)].tolist() == recent
+        union = set(range(max(0, L - w.window), L))
+        for s in recent:
+            union.update(before["supp"][0, s, :before["cnt"][0, s]].tolist())
+        n = int(info.n_cand[0])
+        assert info.cand[0, :n].tolist() == sorted(union)
+
+    _run(w, tiny, p, check=check)
+    assert seen["reuse"] > 10 and seen["fallback"] > 0
+
+
+def test_recent_r_equals_similarity_when_all_entries_are_retrieved(oracle_lib, tiny):
+    """With R = C both retrieval rules retrieve every cached entry, so the two
+    trajectories coincide step for step (same paths, supports and outputs)."""
+    w = tiny.w
+    a = _run(w, tiny, _workload_params(w, r=w.cache_cap))[1]
+    b = _run(w, tiny, _workload_params(w, r=w.cache_cap, retrieval=1))[1]
+    for (oa, sa, ia), (ob, sb, ib) in zip(a, b):
+        assert np.array_equal(ia.path, ib.path)
+        assert np.array_equal(sa, sb)
+        assert np.array_equal(oa, ob)
