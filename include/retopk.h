@@ -77,6 +77,10 @@ typedef struct {
     float   tau;         /* fallback threshold on rho_max, finite                */
     int32_t refresh;     /* T_r (paper), P: refresh period in steps, 0 = off     */
     int32_t dtype;       /* retopk_dtype of q, k and v                           */
+    int32_t retrieval;   /* 0: the R most similar cached queries (Eq. 7); 1: the  */
+                         /* R most recently inserted entries (the recent-R      */
+                         /* alternative of the component ablation, Table 3),    */
+                         /* whose best similarity is then rho_max (Eq. 13)      */
 } retopk_config;
 
 /* Cumulative counters since retopk_create (or the last retopk_set_state). */

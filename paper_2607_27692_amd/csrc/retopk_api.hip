@@ -67,6 +67,7 @@ retopk_status validate_config(const retopk_config *c)
     if (c->k < 1 || c->cache_cap < 0 || c->r < 1 || c->window < 0 || c->refresh < 0)
         return RETOPK_ERR_ARG;
     if (!std::isfinite(c->tau)) return RETOPK_ERR_ARG;
+    if (c->retrieval != 0 && c->retrieval != 1) return RETOPK_ERR_ARG;
     if (c->k > kMaxK || c->cache_cap > kMaxCache || c->r > kMaxR) return RETOPK_ERR_UNSUPPORTED;
     if ((int64_t)c->batch * c->n_q_heads > kMaxHeads) return RETOPK_ERR_UNSUPPORTED;
     if ((int64_t)c->r * c->k + c->window >= ((int64_t)1 << 30)) return RETOPK_ERR_UNSUPPORTED;
@@ -112,6 +113,7 @@ StepArgs base_args(const retopk_handle_s *h)
     a.n_regions = (int)ceil_div(c.max_len, kFilterRows);
     a.row_stride = (int64_t)a.n_regions * kFilterRows;
     a.tau = c.tau;
+    a.retrieval = c.retrieval;
     a.inv_sqrt_d = h->inv_sqrt_d;
     a.q_head_stride = c.head_dim;
     return a;

@@ -83,6 +83,7 @@ struct StepArgs {
     int n_regions;             // ceil(max_len / kFilterRows): surv_cnt row length
     int64_t row_stride;        // n_regions * kFilterRows: row length of scores and surv
     float tau;
+    int retrieval;             // 0: R most similar entries (Eq. 7); 1: R most recent
     float inv_sqrt_d;          // fl32(1 / sqrt(d))
     int mode;
     const void *q;             // element (b, h, e) at q[(b*Hq + h) * q_head_stride + e]

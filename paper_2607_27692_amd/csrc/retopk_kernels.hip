@@ -321,8 +321,11 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
 
     // This block's Top-R slots (Eq. 7) by rank counting: the 4 lanes of a quad
     // compare slot `local` against 16 slots each; rank = number of slots that are
-    // more similar, or equally similar and newer.  The global Top-R is contained
-    // in the union of the blocks' lists.
+    // more similar, or equally similar and newer (with recent-R retrieval: that
+    // are newer).  The global Top-R is contained in the union of the blocks'
+    // lists.  The block's maximum of rho over the entries retrieval can use goes
+    // to rho_bmax: every valid slot for Eq. 7, the R most recent for recent-R.
+    const bool recent = a.retrieval == 1;
     {
         const double ri = s_rho[local];
         const int ai = s_age[local];
@@ -330,19 +333,37 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
 #pragma unroll
         for (int u = 0; u < 16; ++u) {
             const int o = p * 16 + u;
-            cnt += better(s_rho[o], s_age[o], ri, ai) ? 1 : 0;
+            cnt += (recent ? s_age[o] < ai : better(s_rho[o], s_age[o], ri, ai)) ? 1 : 0;
         }
         cnt += __builtin_amdgcn_mov_dpp(cnt, kQuadXor1, 0xF, 0xF, true);
         cnt += __builtin_amdgcn_mov_dpp(cnt, kQuadXor2, 0xF, 0xF, true);
         const int64_t base = ((int64_t)bh * (kMaxCache / kSimSlots) + sb) * kMaxR;
-        if (p == 0 && slot < n_valid && cnt < a.R) {
+        const bool listed = slot < n_valid && cnt < a.R && (!recent || ai < a.R);
+        if (p == 0 && listed) {
             w.topr[base + cnt] = slot;
             w.topr_rho[base + cnt] = ri;
             w.topr_cnt[base + cnt] = scnt;
-            if (cnt == 0) w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = ri;
+            if (cnt == 0 && !recent) w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = ri;
         }
-        if (tid == 0 && sb * kSimSlots >= n_valid)
+        if (tid == 0 && sb * kSimSlots >= n_valid && !recent)
             w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = -INFINITY;
+    }
+    if (recent && wave == 0) {
+        // one lane per slot of the block; list positions past this block's
+        // retrieved entries are marked empty
+        static_assert(kSimSlots == 64, "one lane per slot");
+        const bool ret = sb * kSimSlots + lane < n_valid && s_age[lane] < a.R;
+        double m = ret ? s_rho[lane] : -INFINITY;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+        const int listed = __popcll(__ballot(ret));
+        const int64_t base = ((int64_t)bh * (kMaxCache / kSimSlots) + sb) * kMaxR;
+        if (lane >= listed && lane < a.R) {
+            w.topr[base + lane] = -1;
+            w.topr_rho[base + lane] = -INFINITY;
+            w.topr_cnt[base + lane] = 0;
+        }
+        if (lane == 0) w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = m;
     }
 }
 
@@ -572,7 +593,7 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     __shared__ uint32_t s_red32[NT / 64];
     __shared__ int32_t s_ret[kMaxR];
     __shared__ int32_t s_retcnt[kMaxR];
-    __shared__ double s_mx;
+    __shared__ double s_retrho[kMaxR];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
     const int bh = cb / kCandRanges, s = cb % kCandRanges;
     const int M = a.M;
@@ -599,13 +620,13 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
         const int32_t sl = w.topr[src];
         const double rr = w.topr_rho[src];
         const int32_t cn = w.topr_cnt[src];
-        c_slot[c] = valid ? sl : -1;
-        c_rho[c] = valid ? rr : -INFINITY;
-        c_cnt[c] = valid ? cn : 0;
-        c_age[c] = valid ? slot_age(age0, sl, M) : 0x7FFFFFFF;
+        const bool use = valid && sl >= 0;     // recent-R lists can be shorter
+        c_slot[c] = use ? sl : -1;
+        c_rho[c] = use ? rr : -INFINITY;
+        c_cnt[c] = use ? cn : 0;
+        c_age[c] = use ? slot_age(age0, sl, M) : 0x7FFFFFFF;
         c_rank[c] = 0;
     }
-    if (tid == 0) s_mx = -INFINITY;
     uint4 qv[R::kNV];
     {
         const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)bh * a.q_head_stride);
@@ -616,8 +637,8 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
 
     // Eq. 7: merge the blocks' Top-R lists.  The global rank of candidate c is
     // its position in its own list plus, for every other list, the number of
-    // entries that are more similar, or equally similar and newer; one thread
-    // counts one (candidate, list) pair.  The rank-0 candidate gives rho_max.
+    // entries that are more similar, or equally similar and newer (for recent-R
+    // retrieval: that are newer); one thread counts one (candidate, list) pair.
     for (int pr = tid; pr < nc * nsb; pr += NT) {
         const int c = pr / nsb, o = pr - c * nsb;
         const int32_t sl = c_slot[c];
@@ -638,7 +659,8 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const bool beats = (rr[u] > rc) | ((rr[u] == rc) & (aa[u] < ac));
+                const bool beats = a.retrieval == 1 ? (aa[u] < ac)
+                                                    : ((rr[u] > rc) | ((rr[u] == rc) & (aa[u] < ac)));
                 cnt += (beats & (k0 + u < per)) ? 1 : 0;
             }
         }
@@ -652,13 +674,15 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
         if (rank < nret_all) {
             s_ret[rank] = sl;
             s_retcnt[rank] = c_cnt[c];
+            s_retrho[rank] = c_rho[c];
         }
-        if (rank == 0) s_mx = c_rho[c];
     }
     __syncthreads();
 
-    // rho_max and the path (Eq. 13).
-    const double mx = s_mx;
+    // rho_max, the best similarity among the retrieved entries (for Eq. 7 the
+    // most similar entry of all), and the path (Eq. 13).
+    double mx = -INFINITY;
+    for (int i = 0; i < nret_all; ++i) mx = fmax(mx, s_retrho[i]);
     const int8_t path = mx < (double)a.tau ? PATH_FALLBACK : PATH_REUSE;
     const int nret = path == PATH_REUSE ? nret_all : 0;
     if (s == 0 && tid == 0) {

@@ -35,7 +35,8 @@ class retopk_config(C.Structure):
     _fields_ = [("batch", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
                 ("head_dim", C.c_int32), ("max_len", C.c_int64), ("k", C.c_int32),
                 ("cache_cap", C.c_int32), ("r", C.c_int32), ("window", C.c_int32),
-                ("tau", C.c_float), ("refresh", C.c_int32), ("dtype", C.c_int32)]
+                ("tau", C.c_float), ("refresh", C.c_int32), ("dtype", C.c_int32),
+                ("retrieval", C.c_int32)]
 
 
 class retopk_stats_t(C.Structure):
@@ -109,10 +110,10 @@ def _check(fn: str, rc: int):
 
 
 def make_config(batch, n_q_heads, n_kv_heads, head_dim, max_len, k, cache_cap, r, window, tau,
-                refresh, dtype) -> retopk_config:
+                refresh, dtype, retrieval=0) -> retopk_config:
     dt = {"f32": RETOPK_F32, "bf16": RETOPK_BF16}.get(dtype, dtype)
     return retopk_config(batch, n_q_heads, n_kv_heads, head_dim, max_len, k, cache_cap, r,
-                         window, tau, refresh, dt)
+                         window, tau, refresh, dt, retrieval)
 
 
 # ---------------------------------------------------------------------------

@@ -49,7 +49,8 @@ def handle_of(p: O.Params, dtype: str):
     from paper_2607_27692_amd import retopk as R
     return R.Handle(batch=p.batch, n_q_heads=p.n_q_heads, n_kv_heads=p.n_kv_heads,
                     head_dim=p.head_dim, max_len=p.max_len, k=p.k, cache_cap=p.cache_cap,
-                    r=p.r, window=p.window, tau=p.tau, refresh=p.refresh, dtype=dtype)
+                    r=p.r, window=p.window, tau=p.tau, refresh=p.refresh, dtype=dtype,
+                    retrieval=p.retrieval)
 
 
 def debug_buffers(p: O.Params):

@@ -234,24 +234,26 @@ def test_determinism_16k():
 
 
 VARIANTS = [
-    ("r1", dict(r=1)),                 # a single retrieved entry
-    ("c1", dict(cache_cap=1)),         # a one-entry cache
-    ("tau_minus1", dict(tau=-1.0)),    # never falls back
-    ("no_refresh", dict(refresh=0)),   # refresh off
-    ("no_window", dict(window=0)),     # supports only; fewer than K candidates occur
-    ("always_fallback", dict(tau=2.0)),
+    ("recent_r", {}, dict(retrieval=1)),   # the R most recent entries instead of Eq. 7
+    ("r1", dict(r=1), {}),                 # a single retrieved entry
+    ("c1", dict(cache_cap=1), {}),         # a one-entry cache
+    ("tau_minus1", dict(tau=-1.0), {}),    # never falls back
+    ("no_refresh", dict(refresh=0), {}),   # refresh off
+    ("no_window", dict(window=0), {}),     # supports only; fewer than K candidates occur
+    ("always_fallback", dict(tau=2.0), {}),
 ]
 
 
-@pytest.mark.parametrize("label, change", VARIANTS, ids=[v[0] for v in VARIANTS])
-def test_decode_lockstep_variants(label, change):
-    """The ablation settings of the paper's component study (single retrieved
-    entry, one-entry cache, no fallback, no refresh, no recent window) and the
-    all-fallback limit, on the fp32 single-head workload, all steps in lock-step."""
+@pytest.mark.parametrize("label, change, extra", VARIANTS, ids=[v[0] for v in VARIANTS])
+def test_decode_lockstep_variants(label, change, extra):
+    """The settings of the paper's component ablation (Table 3: recent-R retrieval,
+    a single retrieved entry, a one-entry cache, no fallback, no refresh, no
+    recent window) and the all-fallback limit, on the fp32 single-head workload,
+    all steps in lock-step."""
     w = WORKLOADS["tiny"].with_(**change)
     print(f"decode lock-step {w.name} {label}", flush=True)
     inp = make_inputs(w)
-    p = params_of(w)
+    p = params_of(w, **extra)
     tally, paths = _lockstep(w, inp, p, [0], w.steps)
     print(tally, flush=True)
     assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == w.steps
