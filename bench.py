@@ -53,6 +53,12 @@ def parse():
                     help="no GPU work: turn the csv output of a rocprofv3 kernel-trace run and "
                          "of a FETCH_SIZE and a WRITE_SIZE counter run of this script (with "
                          "--copy-calibration) into the text summaries under profiles/")
+    ap.add_argument("--fidelity", type=int, default=0, metavar="STEPS",
+                    help="instead of timing, run STEPS decode steps from the prefill "
+                         "initialisation and report how close ReTopK's supports and outputs "
+                         "are to Exact Top-K's and to full attention's (support recall, "
+                         "retained attention mass, output cosine), overall and on the "
+                         "reuse path")
     return ap.parse_args()
 
 
@@ -69,6 +75,9 @@ def main():
         print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); the "
               "multi-GPU layout is a design note only", file=sys.stderr)
         sys.exit(2)
+    if args.fidelity:
+        fidelity(args)
+        return
     import torch
 
     from paper_2607_27692_amd import retopk as R
@@ -342,6 +351,107 @@ def cpu_baseline(w, inp, seconds: float):
                        f"0, {n_st} ReTopK steps from a seeded cache state and {n_ex} Exact "
                        f"Top-K steps, scaled x{scale:g} to all heads"),
             "cpu": platform.processor() or platform.machine()}
+
+
+# ---- fidelity diagnostics ------------------------------------------------------
+def support_recall(sel, exact_sel) -> float:
+    """|S_hat & S| / |S| for two -1 padded supports (the overlap measure of Eq. 2
+    applied to the selected and the exact support)."""
+    a = set(int(i) for i in sel if i >= 0)
+    b = set(int(i) for i in exact_sel if i >= 0)
+    return len(a & b) / max(len(b), 1)
+
+
+def retained_mass(sel, probs) -> float:
+    """Share of the full-attention probability mass on the selected positions."""
+    idx = np.asarray([i for i in sel if i >= 0], dtype=np.int64)
+    return float(np.asarray(probs, np.float64)[idx].sum())
+
+
+def cosine(x, y) -> float:
+    x = np.asarray(x, np.float64).ravel()
+    y = np.asarray(y, np.float64).ravel()
+    den = np.linalg.norm(x) * np.linalg.norm(y)
+    return float(x @ y / den) if den > 0 else 1.0
+
+
+def fidelity(args):
+    """ReTopK against Exact Top-K and full attention on the GPU, step by step from
+    the prefill initialisation: support recall (Eq. 2), retained attention mass,
+    attention-distribution cosine and head-output cosine, as the paper reports
+    them for its fidelity analysis (Sec. 4.2)."""
+    import torch
+
+    from paper_2607_27692_amd import retopk as R
+    from paper_2607_27692_amd.inputs import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    steps = min(args.fidelity, w.steps)
+    torch.cuda.set_device(0)
+    inp = make_inputs(w)
+
+    def dev(raw):
+        if raw.dtype == np.uint16:
+            return torch.from_numpy(raw.view(np.int16)).to("cuda")
+        return torch.from_numpy(raw).to("cuda")
+
+    q_tail, q_dec, k, v = (dev(inp.q_tail_raw), dev(inp.q_dec_raw), dev(inp.k_raw),
+                           dev(inp.v_raw))
+    cfg = dict(batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+               head_dim=w.head_dim, max_len=w.max_len, k=w.k, cache_cap=w.cache_cap, r=w.r,
+               window=w.window, tau=w.tau, refresh=w.refresh, dtype=w.dtype)
+    h = R.Handle(**cfg)
+    h.prefill_init(q_tail, w.cache_cap, k, v, w.prompt_len)
+    BH = w.batch * w.n_q_heads
+    out_r = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    out_e = torch.empty_like(out_r)
+    sel_r = torch.empty((w.batch, w.n_q_heads, w.k), dtype=torch.int32, device="cuda")
+    sel_e = torch.empty_like(sel_r)
+    path = torch.empty(BH, dtype=torch.int8, device="cuda")
+    scale = 1.0 / np.sqrt(w.head_dim)
+    rows = []   # (path, recall, mass_r, mass_e, dist_cos, out_cos_exact, out_cos_full)
+    for t in range(steps):
+        L = w.step_len(t)
+        h.decode_step(q_dec[t], k, v, L, out_r, sel_r, {"path": path})
+        h.exact(q_dec[t], k, v, L, out_e, sel_e)
+        torch.cuda.synchronize()
+        sr, se = sel_r.cpu().numpy(), sel_e.cpu().numpy()
+        orr, oe = out_r.cpu().numpy(), out_e.cpu().numpy()
+        pth = path.cpu().numpy()
+        for b in range(w.batch):
+            for g in range(w.n_kv_heads):
+                # full attention in fp32 as the reference
+                as32 = (lambda x: x.view(torch.bfloat16).float()) if w.dtype == "bf16" else (
+                    lambda x: x.float())
+                kf, vf = as32(k[b, g, :L]), as32(v[b, g, :L])
+                qf = as32(q_dec[t][b, g * w.group:(g + 1) * w.group])
+                probs = torch.softmax((qf @ kf.T) * scale, dim=-1)
+                full = (probs @ vf).cpu().numpy()
+                probs = probs.cpu().numpy()
+                for j in range(w.group):
+                    hq = g * w.group + j
+                    sel = sr[b, hq]
+                    idx = sel[sel >= 0]
+                    sparse = np.zeros(L)
+                    sparse[idx] = probs[j][idx] / probs[j][idx].sum()
+                    rows.append((int(pth[b * w.n_q_heads + hq]), support_recall(sel, se[b, hq]),
+                                 retained_mass(sel, probs[j]), retained_mass(se[b, hq], probs[j]),
+                                 cosine(sparse, probs[j]), cosine(orr[b, hq], oe[b, hq]),
+                                 cosine(orr[b, hq], full[j])))
+        log(f"[fidelity] step {t + 1}/{steps}")
+    h.close()
+    a = np.array(rows, dtype=np.float64)
+    names = ["support_recall", "retained_mass", "exact_retained_mass",
+             "attention_distribution_cosine", "output_cosine_vs_exact", "output_cosine_vs_full"]
+
+    def summary(mask):
+        return {n: round(float(a[mask, i + 1].mean()), 5) for i, n in enumerate(names)} | {
+            "head_steps": int(mask.sum())}
+
+    reuse = a[:, 0] == 0   # RETOPK_REUSE
+    print(json.dumps({"fidelity": {"workload": w.name, "steps": steps, "data": "synthetic",
+                                   "all": summary(np.ones(len(a), bool)),
+                                   "reuse_path": summary(reuse)}}), flush=True)
 
 
 # ---- profiler summaries -------------------------------------------------------
