@@ -146,16 +146,20 @@ def main():
 
     retopk_run = lambda hh, t: hh.decode_step(q_dec[t], k, v, w.step_len(t), out, sel)  # noqa
     exact_run = lambda hh, t: hh.exact(q_dec[t], k, v, w.step_len(t), out, sel)  # noqa
+    full_run = lambda hh, t: hh.full(q_dec[t], k, v, w.step_len(t), out)  # noqa
 
     # ---- ReTopK, then the Exact Top-K baseline on the same queries and lengths ---
     r_ms, r_wall, _, st = timed(retopk_run, False)
     log(f"[bench] ReTopK: {r_ms.mean() * 1e3:.1f} us/step (median {np.median(r_ms) * 1e3:.1f})")
     e_ms, e_wall, _, _ = timed(exact_run, False)
     log(f"[bench] Exact: {e_ms.mean() * 1e3:.1f} us/step (median {np.median(e_ms) * 1e3:.1f})")
+    f_ms, _, _, _ = timed(full_run, False)
+    log(f"[bench] Full attention: {f_ms.mean() * 1e3:.1f} us/step")
     # Same passes again with every kernel dispatch timed (events attached to the
     # dispatch packets); the trajectory is deterministic, so the kernels match.
     _, _, r_prof, st_p = timed(retopk_run, True)
     _, _, e_prof, _ = timed(exact_run, True)
+    _, _, f_prof, _ = timed(full_run, True)
     assert st_p == st, "profiled pass diverged from the timed pass"
 
     # ---- algorithmic bytes ------------------------------------------------------
@@ -227,6 +231,19 @@ def main():
                       "bytes_per_launch": round(scan_bytes / launches),
                       "avg_launch_us": round(tot_ms / launches * 1e3, 2)}
 
+    # Full attention: every key and value row once per step.
+    f_us = f_ms.mean() * 1e3
+    full_bytes = w.batch * w.n_kv_heads * mean_len * d * e * 2 + BH * (d * e + d * 4)
+    full_roof = None
+    if f_prof and f_prof.get("dense_chunk", (0, 0))[0]:
+        launches, tot_ms = f_prof["dense_chunk"]
+        fb = K_steps * w.batch * w.n_kv_heads * mean_len * d * e * 2
+        ach = fb / (tot_ms * 1e-3) / 1e9
+        full_roof = {"kernel": "dense_chunk", "bound": "hbm", "achieved": round(ach, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                     "avg_launch_us": round(tot_ms / launches * 1e3, 2),
+                     "bytes_per_launch": round(fb / launches)}
+
     # ---- CPU baseline: the oracle on a bounded sample ------------------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -252,6 +269,9 @@ def main():
                    "cache_state": "warm" if args.warm else "cold (1 GiB read between steps)"},
         "speedup_vs_exact": round(e_us / r_us, 3),
         "exact_us_per_step": round(e_us, 2),
+        "full_attention_us_per_step": round(f_us, 2),
+        "speedup_vs_full_attention": round(f_us / r_us, 3),
+        "full_hbm_frac": round(full_bytes / (f_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         "retopk_us_median": round(float(np.median(r_ms)) * 1e3, 2),
         "exact_us_median": round(float(np.median(e_ms)) * 1e3, 2),
         "fallback_rate": round(fallback / head_steps, 4) if head_steps else None,
@@ -271,6 +291,7 @@ def main():
                           for n, (l, ms) in e_prof.items()},
         "roofline": roof,
         "exact_roofline": exact_roof,
+        "full_attention_roofline": full_roof,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

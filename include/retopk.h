@@ -133,6 +133,15 @@ retopk_status retopk_decode_step(retopk_handle h, const void *q, const void *k, 
                                  int64_t len, float *out, int32_t *sel,
                                  const retopk_debug *dbg, void *stream);
 
+/* Full (dense) attention for every head over rows [0, len): softmax of the scaled
+ * scores of Eq. 4 over all rows, then the weighted sum of the value rows; the
+ * no-selection reference of the paper's comparisons.  Same argument rules as
+ * exact_topk_attention (device pointers, 16-byte aligned, 1 <= len <= max_len);
+ * writes out (float32 [B, Hq, d]) only.  Two kernels: per-chunk partial results
+ * in the handle's workspace, then their merge. */
+retopk_status full_attention(retopk_handle h, const void *q, const void *k, const void *v,
+                             int64_t len, float *out, void *stream);
+
 /* Exact Top-K attention (Eq. 1 with Eq. 4, then Eq. 12) for every head over rows
  * [0, len): the full-history baseline.  Uses the handle's workspaces only; the
  * caches and counters are untouched. */
@@ -167,7 +176,9 @@ retopk_status retopk_set_state(retopk_handle h, const float *qbar, const int32_t
  *   2 retopk_scan    the scoring kernel when every head scans its full history
  *                    (refresh, cold, Exact Top-K, prefill)
  *   3 retopk_filter  threshold bucket and survivor compaction
- *   4 retopk_final   exact Top-K, Softmax-V, cache insert */
+ *   4 retopk_final   exact Top-K, Softmax-V, cache insert
+ *   5 dense_chunk    full_attention: per-chunk softmax and value sums
+ *   6 dense_merge    full_attention: merge of the chunks */
 retopk_status retopk_profile(retopk_handle h, int32_t enable);
 retopk_status retopk_profile_read(retopk_handle h, int32_t n_kernels, uint64_t *launches,
                                   double *total_ms);

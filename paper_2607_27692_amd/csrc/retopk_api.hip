@@ -17,13 +17,15 @@ using namespace retopk;
 namespace {
 
 constexpr int kProfileMaxLaunches = 65536;
-constexpr int kNumKernels = 5;
+constexpr int kNumKernels = 7;
 // retopk_score is the scoring kernel of a decode step that selects (candidate
 // blocks beside the scans of fallback heads); retopk_scan is the same kernel
 // built for steps where every head takes the full-history scan.
 const char *const kKernelNames[kNumKernels] = {"retopk_sim", "retopk_score", "retopk_scan",
-                                               "retopk_filter", "retopk_final"};
-enum { KID_SIM = 0, KID_SCORE = 1, KID_SCAN = 2, KID_FILTER = 3, KID_FINAL = 4 };
+                                               "retopk_filter", "retopk_final", "dense_chunk",
+                                               "dense_merge"};
+enum { KID_SIM = 0, KID_SCORE = 1, KID_SCAN = 2, KID_FILTER = 3, KID_FINAL = 4, KID_DENSE = 5,
+       KID_DENSE_MERGE = 6 };
 
 }  // namespace
 
@@ -111,6 +113,7 @@ StepArgs base_args(const retopk_handle_s *h)
     a.W = c.window;
     a.cand_cap = h->cand_cap;
     a.n_regions = (int)ceil_div(c.max_len, kFilterRows);
+    a.n_dense = (int)ceil_div(c.max_len, kDenseRows);
     a.row_stride = (int64_t)a.n_regions * kFilterRows;
     a.tau = c.tau;
     a.retrieval = c.retrieval;
@@ -161,6 +164,19 @@ retopk_status fail(retopk_handle h)
     return RETOPK_ERR_HIP;
 }
 
+// Launches one described kernel on s (events attached to its dispatch when
+// profiling).
+retopk_status launch_desc(retopk_handle h, const KernelDesc &d, int kid, void **args, hipStream_t s)
+{
+    hipEvent_t start, stop;
+    retopk_status st = timing_for(h, kid, &start, &stop);
+    if (st != RETOPK_OK) return st;
+    hipError_t e = start
+        ? hipExtLaunchKernel(d.func, d.grid, d.block, args, d.lds_bytes, s, start, stop, 0)
+        : hipLaunchKernel(d.func, d.grid, d.block, args, d.lds_bytes, s);
+    return e == hipSuccess ? RETOPK_OK : fail(h);
+}
+
 // Launches one step (or one prefill query) in `mode`: SELECT runs k_sim, k_score,
 // k_filter, k_final; the other modes k_score (scan only), k_filter, k_final.
 // With profiling on, events are attached to each kernel's dispatch.
@@ -185,14 +201,8 @@ retopk_status run_step(retopk_handle h, const StepArgs &a, int mode, hipStream_t
         if (kinds[i] == KERNEL_SIM) kid = KID_SIM;
         else if (kinds[i] == KERNEL_SCORE) kid = mode == MODE_SELECT ? KID_SCORE : KID_SCAN;
         else if (kinds[i] == KERNEL_FILTER) kid = KID_FILTER;
-        hipEvent_t start, stop;
-        retopk_status st = timing_for(h, kid, &start, &stop);
+        retopk_status st = launch_desc(h, d[i], kid, args, s);
         if (st != RETOPK_OK) return st;
-        hipError_t e = start
-            ? hipExtLaunchKernel(d[i].func, d[i].grid, d[i].block, args, d[i].lds_bytes, s, start,
-                                 stop, 0)
-            : hipLaunchKernel(d[i].func, d[i].grid, d[i].block, args, d[i].lds_bytes, s);
-        if (e != hipSuccess) return fail(h);
     }
     return RETOPK_OK;
 }
@@ -263,7 +273,9 @@ retopk_status retopk_create(const retopk_config *cfg, retopk_handle *out)
         (st = alloc(h, &w.surv_cnt, (size_t)(BH * NR))) != RETOPK_OK ||
         (st = alloc(h, &w.cand_ent, (size_t)(BH * kCandRanges * h->cand_cap))) != RETOPK_OK ||
         (st = alloc(h, &w.cand_cnt, (size_t)(BH * kCandRanges))) != RETOPK_OK ||
-        (st = alloc(h, &w.stats, (size_t)STAT_COUNT)) != RETOPK_OK) {
+        (st = alloc(h, &w.stats, (size_t)STAT_COUNT)) != RETOPK_OK ||
+        (st = alloc(h, &w.dense_part, (size_t)(BH * ceil_div(cfg->max_len, kDenseRows) *
+                                                (cfg->head_dim + 2)))) != RETOPK_OK) {
         retopk_destroy(h);
         return st;
     }
@@ -389,6 +401,36 @@ retopk_status retopk_prefill_init(retopk_handle h, const void *q_tail, int32_t n
         if (st != RETOPK_OK) return st;
         h->n_ins += 1;
     }
+    h->last_stream = s;
+    return RETOPK_OK;
+}
+
+retopk_status full_attention(retopk_handle h, const void *q, const void *k, const void *v,
+                             int64_t len, float *out, void *stream)
+{
+    if (!h || !q || !k || !v || !out) return RETOPK_ERR_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out)) return RETOPK_ERR_ARG;
+    if (len < 1 || len > h->cfg.max_len) return RETOPK_ERR_ARG;
+    if (h->broken) return RETOPK_ERR_STATE;
+    StepArgs a = base_args(h);
+    a.mode = MODE_EXACT;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.len = len;
+    a.out = out;
+    a.do_insert = 0;
+    hipStream_t s = (hipStream_t)stream;
+    if (hipSetDevice(h->device) != hipSuccess) return fail(h);
+    const Geometry geo = make_geometry(h, len, MODE_EXACT);
+    Ws wv = h->w;
+    void *args[3] = {&a, &wv, nullptr};
+    KernelDesc d;
+    describe_kernel(KERNEL_DENSE, h->cfg.dtype, a, geo, &d);
+    retopk_status st = launch_desc(h, d, KID_DENSE, args, s);
+    if (st != RETOPK_OK) return st;
+    describe_kernel(KERNEL_DENSE_MERGE, h->cfg.dtype, a, geo, &d);
+    if ((st = launch_desc(h, d, KID_DENSE_MERGE, args, s)) != RETOPK_OK) return st;
     h->last_stream = s;
     return RETOPK_OK;
 }

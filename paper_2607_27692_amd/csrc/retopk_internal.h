@@ -72,6 +72,7 @@ struct Ws {
     uint64_t *cand_ent;   // [BH, kCandRanges, cand_cap] candidate rank entries per range
     uint32_t *cand_cnt;   // [BH, kCandRanges]
     unsigned long long *stats;  // [STAT_COUNT]
+    float *dense_part;    // [BH, n_dense_chunks, d + 2] full attention: o, m, l per chunk
 };
 
 // Everything one launch needs (passed by value).
@@ -81,6 +82,7 @@ struct StepArgs {
     int K, M, R, W;
     int cand_cap;
     int n_regions;             // ceil(max_len / kFilterRows): surv_cnt row length
+    int n_dense;               // ceil(max_len / kDenseRows): dense_part chunks per head
     int64_t row_stride;        // n_regions * kFilterRows: row length of scores and surv
     float tau;
     int retrieval;             // 0: R most similar entries (Eq. 7); 1: R most recent
@@ -121,7 +123,12 @@ struct KernelDesc {
     unsigned lds_bytes;      // dynamic LDS
     int nargs;
 };
-enum : int { KERNEL_SIM = 0, KERNEL_SCORE = 1, KERNEL_FILTER = 2, KERNEL_FINAL = 3 };
+enum : int { KERNEL_SIM = 0, KERNEL_SCORE = 1, KERNEL_FILTER = 2, KERNEL_FINAL = 3,
+              KERNEL_DENSE = 4, KERNEL_DENSE_MERGE = 5 };
+
+// Full (dense) attention: rows per chunk block, and the chunk count for a length.
+constexpr int kDenseRows = 1024;
+constexpr int kDenseThreads = 512;
 
 // Fills *k for kernel `which` of a step in a.mode (retopk_kernels.hip).
 // dtype: 0 = f32, 1 = bf16.

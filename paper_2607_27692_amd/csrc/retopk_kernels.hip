@@ -1342,6 +1342,232 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
 }
 
 // ---------------------------------------------------------------------------
+// Full attention (the dense baseline): softmax over every row, then V
+// ---------------------------------------------------------------------------
+
+// k_dense: block (b, g, c) takes rows [c * kDenseRows, ...) of KV group (b, g) for
+// the G query heads of the group (one key or value row load serves all of them):
+// scores with the scan's row geometry, then per head the chunk's maximum m, the
+// weights exp(s - m), their sum l and the weighted sum o of the value rows.
+// (o, m, l) go to dense_part; k_dense_merge rescales and adds the chunks.
+template <typename T, int D, int G>
+__global__ __launch_bounds__(kDenseThreads, 4) void k_dense(StepArgs a, Ws w)
+{
+    using R = RowT<T, D>;
+    constexpr int NT = kDenseThreads, NW = NT / 64;
+    constexpr int VL = D * (int)sizeof(T) / 16;     // lanes per value row (16 bytes each)
+    constexpr int VR = 64 / VL;                      // value rows per wave instruction
+    constexpr int EPV = 16 / (int)sizeof(T);
+    static_assert(VL >= 1 && VL <= 64 && 64 % VL == 0, "value row geometry");
+    __shared__ float s_sc[G][kDenseRows];
+    __shared__ float s_red[NW][G];
+    __shared__ float s_o[NW][G][D];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
+    const int nch = (int)((a.len + kDenseRows - 1) / kDenseRows);
+    const int c = blockIdx.x % nch, bg = blockIdx.x / nch;
+    const int b = bg / a.Hkv, g = bg % a.Hkv;
+    const int bh0 = b * a.Hq + g * G;
+    const int64_t r0 = (int64_t)c * kDenseRows;
+    const int nrow = (int)(a.len - r0 < kDenseRows ? a.len - r0 : kDenseRows);
+    const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
+    const T *vbase = (const T *)a.v + ((int64_t)b * a.Hkv + g) * a.max_len * D;
+
+    uint4 qv[G][R::kNV];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)(bh0 + j) * a.q_head_stride);
+#pragma unroll
+        for (int v = 0; v < R::kNV; ++v) qv[j][v] = qr[v * 4 + p];
+    }
+    // scores (Eq. 4) of the chunk's rows, two rows per lane per pass
+    for (int base = 0; base < nrow; base += 2 * kScanRowsPerIter) {
+        uint4 kv[2][R::kNV];
+        int row[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            row[u] = base + u * kScanRowsPerIter + wave * 16 + rl;
+            const uint4 *rp = (const uint4 *)(kbase + (r0 + (row[u] < nrow ? row[u] : 0)) * D);
+#pragma unroll
+            for (int v = 0; v < R::kNV; ++v) kv[u][v] = rp[v * 4 + p];
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            float acc[G];
+#pragma unroll
+            for (int j = 0; j < G; ++j) {
+                float s0 = 0.0f;
+#pragma unroll
+                for (int v = 0; v < R::kNV; ++v) s0 = Dot<T>::f(kv[u][v], qv[j][v], s0);
+                acc[j] = s0;
+            }
+            float sc_lo, sc_hi;
+            group_scores<G>(acc, p, sc_lo, sc_hi);
+            if (row[u] < nrow) {
+#pragma unroll
+                for (int jj = 0; jj < (G + 3) / 4; ++jj) {
+                    const int j = jj * 4 + (G == 1 ? 0 : (G == 2 ? (p & 1) : p));
+                    const bool mine = G == 1 ? p == 0 : (G == 2 ? p < 2 : true);
+                    if (mine) s_sc[j][row[u]] = (jj == 0 ? sc_lo : sc_hi) * a.inv_sqrt_d;
+                }
+            }
+        }
+    }
+    __syncthreads();
+    // per head: chunk maximum, then weights exp(s - m) in place and their sum
+    float m[G], l[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        float x = -INFINITY;
+        for (int i = tid; i < nrow; i += NT) x = fmaxf(x, s_sc[j][i]);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+        if (lane == 0) s_red[wave][j] = x;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        m[j] = s_red[0][j];
+#pragma unroll
+        for (int i = 1; i < NW; ++i) m[j] = fmaxf(m[j], s_red[i][j]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        float x = 0.0f;
+        for (int i = tid; i < nrow; i += NT) {
+            const float e = expf(s_sc[j][i] - m[j]);
+            s_sc[j][i] = e;
+            x += e;
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+        if (lane == 0) s_red[wave][j] = x;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        l[j] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) l[j] += s_red[i][j];
+    }
+    // Eq. 12 over the chunk: VL lanes per value row, each holding EPV elements
+    // for every head; rows spread over the waves.
+    const int sub = lane / VL, vl = lane % VL;
+    float acc[G][EPV];
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) acc[j][e] = 0.0f;
+    for (int t0 = wave * VR; t0 < nrow; t0 += NW * VR * 4) {
+        uint4 raw[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int t = t0 + u * NW * VR + sub;
+            raw[u] = ((const uint4 *)(vbase + (r0 + (t < nrow ? t : 0)) * D))[vl];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int t = t0 + u * NW * VR + sub;
+            if (t < nrow) {
+#pragma unroll
+                for (int j = 0; j < G; ++j) Dot<T>::axpy(raw[u], s_sc[j][t], acc[j]);
+            }
+        }
+    }
+#pragma unroll
+    for (int o = VL; o < 64; o <<= 1)
+#pragma unroll
+        for (int j = 0; j < G; ++j)
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) acc[j][e] += __shfl_xor(acc[j][e], o);
+    if (sub == 0)
+#pragma unroll
+        for (int j = 0; j < G; ++j)
+#pragma unroll
+            for (int e = 0; e < EPV; ++e) s_o[wave][j][vl * EPV + e] = acc[j][e];
+    __syncthreads();
+    for (int i = tid; i < G * D; i += NT) {
+        const int j = i / D, e = i % D;
+        float o = 0.0f;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) o += s_o[ww][j][e];
+        float *dst = w.dense_part + ((int64_t)(bh0 + j) * a.n_dense + c) * (D + 2);
+        dst[e] = o;
+        if (e == 0) {
+            dst[D] = m[j];
+            dst[D + 1] = l[j];
+        }
+    }
+}
+
+// k_dense_merge: one block per head; out = sum_c e^(m_c - M) o_c / sum_c e^(m_c - M) l_c
+// with M the largest chunk maximum.  The chunks are spread over the waves, the
+// head dimension over the lanes, with several chunks' loads in flight.
+template <int D>
+__global__ __launch_bounds__(256) void k_dense_merge(StepArgs a, Ws w)
+{
+    constexpr int NT = 256, NW = NT / 64, EPL = D / 64, U = 4;
+    static_assert(D % 64 == 0, "whole elements per lane");
+    __shared__ float s_red[NW];
+    __shared__ float s_o[NW][D];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, bh = blockIdx.x;
+    const int nch = (int)((a.len + kDenseRows - 1) / kDenseRows);
+    const float *part = w.dense_part + (int64_t)bh * a.n_dense * (D + 2);
+    // M, then L = sum_c e^(m_c - M) l_c
+    float mx = -INFINITY;
+    for (int c = tid; c < nch; c += NT) mx = fmaxf(mx, part[(int64_t)c * (D + 2) + D]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    if (lane == 0) s_red[wave] = mx;
+    __syncthreads();
+    float M = s_red[0];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) M = fmaxf(M, s_red[i]);
+    __syncthreads();
+    float l = 0.0f;
+    for (int c = tid; c < nch; c += NT) {
+        const float *pc = part + (int64_t)c * (D + 2);
+        l += expf(pc[D] - M) * pc[D + 1];
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
+    if (lane == 0) s_red[wave] = l;
+    // o: chunk c by wave c % NW, EPL consecutive elements per lane
+    float acc[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[e] = 0.0f;
+    for (int c0 = wave; c0 < nch; c0 += NW * U) {
+        float mv[U], ov[U][EPL];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * NW < nch ? c0 + u * NW : c0;
+            const float *pc = part + (int64_t)c * (D + 2);
+            mv[u] = pc[D];
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) ov[u][e] = pc[lane * EPL + e];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const float f = c0 + u * NW < nch ? expf(mv[u] - M) : 0.0f;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) acc[e] += f * ov[u][e];
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) s_o[wave][lane * EPL + e] = acc[e];
+    __syncthreads();
+    if (tid < D) {
+        float L = 0.0f, o = 0.0f;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) {
+            L += s_red[i];
+            o += s_o[i][tid];
+        }
+        a.out[(int64_t)bh * D + tid] = o / L;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 
@@ -1391,6 +1617,20 @@ static void score_g(const StepArgs &a, const Geometry &geo, KernelDesc *k)
     }
 }
 
+template <typename T, int D>
+static void dense_g(const StepArgs &a, KernelDesc *k)
+{
+    const unsigned blocks = (unsigned)((int64_t)a.B * a.Hkv * ((a.len + kDenseRows - 1) / kDenseRows));
+    const void *f;
+    switch (a.G) {
+    case 1: f = (const void *)&k_dense<T, D, 1>; break;
+    case 2: f = (const void *)&k_dense<T, D, 2>; break;
+    case 4: f = (const void *)&k_dense<T, D, 4>; break;
+    default: f = (const void *)&k_dense<T, D, 8>; break;
+    }
+    *k = KernelDesc{f, dim3(blocks), dim3(kDenseThreads), 0u, 2};
+}
+
 void describe_kernel(int which, int dtype, const StepArgs &a, const Geometry &geo, KernelDesc *k)
 {
     const bool bf = dtype == 1, d64 = a.D == 64;
@@ -1404,6 +1644,13 @@ void describe_kernel(int which, int dtype, const StepArgs &a, const Geometry &ge
     case KERNEL_FILTER:
         *k = KernelDesc{(const void *)&k_filter, dim3((unsigned)(a.B * a.Hq * geo.filter_blocks_per_head)),
                         dim3(kScoreThreads), 0u, 3};
+        return;
+    case KERNEL_DENSE:
+        if (bf) return d64 ? dense_g<uint16_t, 64>(a, k) : dense_g<uint16_t, 128>(a, k);
+        return d64 ? dense_g<float, 64>(a, k) : dense_g<float, 128>(a, k);
+    case KERNEL_DENSE_MERGE:
+        *k = KernelDesc{d64 ? (const void *)&k_dense_merge<64> : (const void *)&k_dense_merge<128>,
+                        dim3((unsigned)(a.B * a.Hq)), dim3(256), 0u, 2};
         return;
     default:
         if (bf) return d64 ? final_desc<uint16_t, 64>(a, k) : final_desc<uint16_t, 128>(a, k);

@@ -20,7 +20,8 @@ STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape", -3: "device 
 
 # Every symbol include/retopk.h declares.
 EXPORTS = ("retopk_create", "retopk_destroy", "retopk_prefill_init", "retopk_decode_step",
-           "exact_topk_attention", "retopk_stats", "retopk_get_state", "retopk_set_state",
+           "exact_topk_attention", "full_attention", "retopk_stats", "retopk_get_state",
+           "retopk_set_state",
            "retopk_profile", "retopk_profile_read", "retopk_kernel_name",
            "retopk_status_string")
 
@@ -70,6 +71,7 @@ def load(path: str | None = None):
         "retopk_prefill_init": ([P, P, I32, P, P, I64, P], C.c_int),
         "retopk_decode_step": ([P, P, P, P, I64, P, P, C.POINTER(retopk_debug), P], C.c_int),
         "exact_topk_attention": ([P, P, P, P, I64, P, P, P], C.c_int),
+        "full_attention": ([P, P, P, P, I64, P, P], C.c_int),
         "retopk_stats": ([P, C.POINTER(retopk_stats_t)], C.c_int),
         "retopk_get_state": ([P, P, P, P, C.POINTER(I64), C.POINTER(I64)], C.c_int),
         "retopk_set_state": ([P, P, P, P, I64, I64], C.c_int),
@@ -150,6 +152,11 @@ def retopk_decode_step(h, q, k, v, length, out, sel=None, dbg: dict | None = Non
 def exact_topk_attention(h, q, k, v, length, out, sel=None, stream=None) -> None:
     _check("exact_topk_attention", load().exact_topk_attention(
         h, _addr(q), _addr(k), _addr(v), length, _addr(out), _addr(sel), _stream(stream)))
+
+
+def full_attention(h, q, k, v, length, out, stream=None) -> None:
+    _check("full_attention", load().full_attention(
+        h, _addr(q), _addr(k), _addr(v), length, _addr(out), _stream(stream)))
 
 
 def retopk_stats(h) -> dict:
@@ -236,6 +243,9 @@ class Handle:
 
     def exact(self, q, k, v, length, out, sel=None, stream=None):
         exact_topk_attention(self.h, q, k, v, length, out, sel, stream)
+
+    def full(self, q, k, v, length, out, stream=None):
+        full_attention(self.h, q, k, v, length, out, stream)
 
     def stats(self):
         return retopk_stats(self.h)

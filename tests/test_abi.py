@@ -37,9 +37,10 @@ def test_every_declared_symbol_is_exported(lib):
 def test_status_strings(lib):
     for code in (0, -1, -2, -3, -4, -5):
         assert R.retopk_status_string(code) == R.STATUS[code]
-    assert [R.retopk_kernel_name(i) for i in range(5)] == [
-        "retopk_sim", "retopk_score", "retopk_scan", "retopk_filter", "retopk_final"]
-    assert R.retopk_kernel_name(5) is None and R.retopk_kernel_name(-1) is None
+    assert [R.retopk_kernel_name(i) for i in range(7)] == [
+        "retopk_sim", "retopk_score", "retopk_scan", "retopk_filter", "retopk_final",
+        "dense_chunk", "dense_merge"]
+    assert R.retopk_kernel_name(7) is None and R.retopk_kernel_name(-1) is None
 
 
 def _cfg(**kw):
@@ -70,6 +71,7 @@ def test_null_arguments(lib):
     assert lib.retopk_destroy(None) == 0
     assert lib.retopk_decode_step(None, 16, 16, 16, 1, 16, None, None, None) == -1
     assert lib.exact_topk_attention(None, 16, 16, 16, 1, 16, None, None) == -1
+    assert lib.full_attention(None, 16, 16, 16, 1, 16, None) == -1
     assert lib.retopk_prefill_init(None, 16, 1, 16, 16, 1, None) == -1
     st = R.retopk_stats_t()
     assert lib.retopk_stats(None, C.byref(st)) == -1
