@@ -59,6 +59,12 @@ def parse():
                          "are to Exact Top-K's and to full attention's (support recall, "
                          "retained attention mass, output cosine), overall and on the "
                          "reuse path")
+    ap.add_argument("--layers", type=int, default=0, metavar="L",
+                    help="instead of the one-layer protocol, decode with L independent layers "
+                         "(each its own keys, values, queries and ReTopK state) one after the "
+                         "other per token, as a model does, and report ms per token over the L "
+                         "layers for ReTopK, Exact Top-K and full attention (no cache flush: "
+                         "rotating the layers' key and value rows defeats the caches)")
     return ap.parse_args()
 
 
@@ -77,6 +83,9 @@ def main():
         sys.exit(2)
     if args.fidelity:
         fidelity(args)
+        return
+    if args.layers:
+        layers(args)
         return
     import torch
 
@@ -116,6 +125,7 @@ def main():
     for t in range(min(args.warmup, w.steps)):
         h.decode_step(q_dec[t], k, v, w.step_len(t), out, sel)
         h.exact(q_dec[t], k, v, w.step_len(t), out, sel)
+        h.full(q_dec[t], k, v, w.step_len(t), out)
     torch.cuda.synchronize()
     h.close()
     log("[bench] warm-up done")
@@ -241,6 +251,7 @@ def main():
         ach = fb / (tot_ms * 1e-3) / 1e9
         full_roof = {"kernel": "dense_chunk", "bound": "hbm", "achieved": round(ach, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                     "traffic": traffic_per_launch("dense_chunk", w.name),
                      "avg_launch_us": round(tot_ms / launches * 1e3, 2),
                      "bytes_per_launch": round(fb / launches)}
 
@@ -475,6 +486,136 @@ def fidelity(args):
                                    "reuse_path": summary(reuse)}}), flush=True)
 
 
+# ---- several layers per token ---------------------------------------------------
+def _layer_inputs(job):
+    """Worker: the raw arrays of one layer (the workload drawn from its own seed)."""
+    from paper_2607_27692_amd.inputs import WORKLOADS, make_inputs
+    name, seed = job
+    inp = make_inputs(WORKLOADS[name], seed=seed)
+    return seed, inp.q_tail_raw, inp.q_dec_raw, inp.k_raw, inp.v_raw
+
+
+def layers(args):
+    """ms per token over L layers: token t runs decode step t of layer 0, 1, ..,
+    L-1 in turn (each layer its own handle, keys, values and queries, layer l
+    drawn from seed l), the way the paper reports decode latency per token over a
+    model's layers (Table 4).  The Exact Top-K and full-attention passes run the
+    same layers and tokens.  Each token is bracketed by HIP events; there is no
+    flush, since L layers' key and value rows exceed the caches."""
+    import multiprocessing as mp
+
+    from paper_2607_27692_amd.inputs import WORKLOADS
+    w = WORKLOADS[args.workload]
+    L = args.layers
+    T = min(args.steps, w.steps)
+    # Generate on the host before this process touches the GPU (the workers are
+    # forked), then upload layer by layer.
+    t0 = time.time()
+    n_proc = max(1, min(L, 16, os.cpu_count() or 1))
+    ctx = mp.get_context("fork")
+    pool = ctx.Pool(n_proc)
+    import torch
+
+    from paper_2607_27692_amd import retopk as R
+    lay = [None] * L
+
+    def dev(raw):
+        if raw.dtype == np.uint16:
+            return torch.from_numpy(raw.view(np.int16)).to("cuda")
+        return torch.from_numpy(raw).to("cuda")
+
+    for seed, qt, qd, kr, vr in pool.imap_unordered(_layer_inputs, [(w.name, l) for l in range(L)]):
+        lay[seed] = (dev(qt), dev(qd), dev(kr), dev(vr))
+        del qt, qd, kr, vr
+        log(f"[layers] layer {seed} resident ({L - lay.count(None)}/{L})")
+    pool.close()
+    pool.join()
+    log(f"[layers] inputs of {L} layers generated and uploaded in {time.time() - t0:.1f}s")
+    torch.cuda.set_device(0)
+    cfg = dict(batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+               head_dim=w.head_dim, max_len=w.max_len, k=w.k, cache_cap=w.cache_cap, r=w.r,
+               window=w.window, tau=w.tau, refresh=w.refresh, dtype=w.dtype)
+    out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    sel = torch.empty((w.batch, w.n_q_heads, w.k), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def handles():
+        hs = []
+        for qt, _, kk, vv in lay:
+            hh = R.Handle(**cfg)
+            hh.prefill_init(qt, w.cache_cap, kk, vv, w.prompt_len)
+            hs.append(hh)
+        torch.cuda.synchronize()
+        return hs
+
+    def decode(hh, l, t):
+        _, qd, kk, vv = lay[l]
+        hh.decode_step(qd[t], kk, vv, w.step_len(t), out, sel)
+
+    def exact(hh, l, t):
+        _, qd, kk, vv = lay[l]
+        hh.exact(qd[t], kk, vv, w.step_len(t), out, sel)
+
+    def full(hh, l, t):
+        _, qd, kk, vv = lay[l]
+        hh.full(qd[t], kk, vv, w.step_len(t), out)
+
+    def run(fn, hs, n_tokens):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(n_tokens)]
+        torch.cuda.synchronize()
+        for t in range(n_tokens):
+            ev[t][0].record(stream)
+            for l in range(L):
+                fn(hs[l], l, t)
+            ev[t][1].record(stream)
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in ev])
+
+    # warm-up on throwaway handles, then fresh handles for the timed ReTopK pass
+    hs = handles()
+    for fn in (decode, exact, full):
+        run(fn, hs, min(args.warmup, T))
+    for hh in hs:
+        hh.close()
+    log("[layers] warm-up done")
+    hs = handles()
+    st0 = [hh.stats() for hh in hs]
+    r_ms = run(decode, hs, T)
+    st = {k_: sum(hh.stats()[k_] - s0[k_] for hh, s0 in zip(hs, st0)) for k_ in st0[0]}
+    log(f"[layers] ReTopK: {r_ms.mean():.3f} ms/token")
+    e_ms = run(exact, hs, T)
+    log(f"[layers] Exact: {e_ms.mean():.3f} ms/token")
+    f_ms = run(full, hs, T)
+    log(f"[layers] Full attention: {f_ms.mean():.3f} ms/token")
+    for hh in hs:
+        hh.close()
+    hsteps = st["head_steps"]
+    print(json.dumps({
+        "metric": f"ms per token over {L} layers (all heads of each layer), "
+                  f"{w.prompt_len // 1024}K ctx, K={w.k}",
+        "value": round(float(r_ms.mean()), 4), "unit": "ms/token", "n_gpus": 1,
+        "layers": L, "tokens": T, "warmup": args.warmup, "higher_is_better": False,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": w.name, "layers": L, "batch": w.batch, "q_heads": w.n_q_heads,
+                   "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "context": w.prompt_len,
+                   "k": w.k, "cache_cap": w.cache_cap, "r": w.r, "window": w.window,
+                   "tau": w.tau, "refresh": w.refresh},
+        "retopk_ms_per_token": round(float(r_ms.mean()), 4),
+        "retopk_ms_median": round(float(np.median(r_ms)), 4),
+        "exact_ms_per_token": round(float(e_ms.mean()), 4),
+        "full_attention_ms_per_token": round(float(f_ms.mean()), 4),
+        "speedup_vs_exact": round(float(e_ms.mean() / r_ms.mean()), 3),
+        "speedup_vs_full_attention": round(float(f_ms.mean() / r_ms.mean()), 3),
+        "retopk_us_per_layer": round(float(r_ms.mean()) * 1e3 / L, 2),
+        "exact_us_per_layer": round(float(e_ms.mean()) * 1e3 / L, 2),
+        "full_attention_us_per_layer": round(float(f_ms.mean()) * 1e3 / L, 2),
+        "fallback_rate": round(st["fallback"] / hsteps, 4) if hsteps else None,
+        "refresh_share": round(st["refresh"] / hsteps, 4) if hsteps else None,
+        "kv_group_scans_per_layer_step": round(st["kv_group_scans"] / (T * L), 3),
+    }), flush=True)
+
+
 # ---- profiler summaries -------------------------------------------------------
 SYMBOLS = {  # kernel symbol prefix -> name used by the library's own profiling
     "void retopk::k_sim<": "retopk_sim",
@@ -482,6 +623,8 @@ SYMBOLS = {  # kernel symbol prefix -> name used by the library's own profiling
     "void retopk::k_score<unsigned short, 128, 4, false>": "retopk_scan",
     "retopk::k_filter(": "retopk_filter",
     "void retopk::k_final<": "retopk_final",
+    "void retopk::k_dense<": "dense_chunk",
+    "void retopk::k_dense_merge<": "dense_merge",
 }
 
 
@@ -502,22 +645,26 @@ def _passes(names, w, steps, warmup):
     """Splits the library's dispatches (in dispatch order) into the bench's
     passes.  Every pass starts on a fresh handle whose prefill issues one
     scan, filter, final triple per prompt-tail query; a decode step that selects
-    issues sim, score, filter, final, any other step scan, filter, final.
-    Returns (label, first, end) positions of each pass's step dispatches."""
-    plan = [("warm-up", 2 * min(warmup, w.steps)), ("retopk timed", steps),
-            ("exact timed", steps), ("retopk profiled", steps), ("exact profiled", steps)]
-    step4 = ["retopk_sim", "retopk_score", "retopk_filter", "retopk_final"]
-    step3 = ["retopk_scan", "retopk_filter", "retopk_final"]
+    issues sim, score, filter, final, any other step or an Exact Top-K step
+    scan, filter, final, and a full-attention step dense_chunk, dense_merge.
+    The warm-up runs one step of each kind per warm-up step.  Returns
+    (label, first, end) positions of each pass's step dispatches."""
+    plan = [("warm-up", 3 * min(warmup, w.steps)), ("retopk timed", steps),
+            ("exact timed", steps), ("full timed", steps), ("retopk profiled", steps),
+            ("exact profiled", steps), ("full profiled", steps)]
+    units = {"retopk_sim": ["retopk_sim", "retopk_score", "retopk_filter", "retopk_final"],
+             "retopk_scan": ["retopk_scan", "retopk_filter", "retopk_final"],
+             "dense_chunk": ["dense_chunk", "dense_merge"]}
     out, i = [], 0
-    for label, n_steps in plan:
+    for label, n_units in plan:
         for _ in range(w.cache_cap):
-            assert names[i:i + 3] == step3, f"unexpected prefill dispatches at {i}"
+            assert names[i:i + 3] == units["retopk_scan"], f"unexpected prefill dispatches at {i}"
             i += 3
         start = i
-        for _ in range(n_steps):
-            n = 4 if names[i] == "retopk_sim" else 3
-            assert names[i:i + n] == (step4 if n == 4 else step3), f"unexpected step at {i}"
-            i += n
+        for _ in range(n_units):
+            unit = units.get(names[i])
+            assert unit and names[i:i + len(unit)] == unit, f"unexpected step at {i}"
+            i += len(unit)
         out.append((label, start, i))
     assert i == len(names), "dispatches left over"
     return out
@@ -542,7 +689,7 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
              "-d <out>/kt -o kt -- python3 -u <repo>/bench.py --no-cpu-baseline",
              "summary: python bench.py --summarize <out>/kt <out>/pmc_fetch <out>/pmc_write",
              "",
-             "## rocprofv3 --stats (every dispatch of the run: prefill, warm-up and the four passes)",
+             "## rocprofv3 --stats (every dispatch of the run: prefill, warm-up and the six passes)",
              f"{'kernel':60s} {'library name':14s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'share':>7s}"]
     for r in stats:
         name = _lib_name(r["Name"]) or ""
@@ -555,7 +702,8 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
         acc = {}
         for r, n in lib[a:b]:
             acc.setdefault(n, []).append(dur(r))
-        for n in ("retopk_sim", "retopk_score", "retopk_scan", "retopk_filter", "retopk_final"):
+        for n in ("retopk_sim", "retopk_score", "retopk_scan", "retopk_filter", "retopk_final",
+                  "dense_chunk", "dense_merge"):
             if n in acc:
                 v = acc[n]
                 lines.append(f"{label:18s} {n:14s} {len(v):8d} {sum(v) / len(v):9.2f}")
@@ -579,7 +727,7 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
     w_factor = copy_kib / (sum(w_big) / len(w_big))
     digest = kernel_source_digest()
     written = [kt_path]
-    for kernel, pass_idx in (("retopk_score", 1), ("retopk_scan", 2)):
+    for kernel, pass_idx in (("retopk_score", 1), ("retopk_scan", 2), ("dense_chunk", 3)):
         _, a, b = passes[pass_idx]
         fv = [v for v, n in fetch[a:b] if n == kernel]
         wv = [v for v, n in write[a:b] if n == kernel]

@@ -129,6 +129,7 @@ enum : int { KERNEL_SIM = 0, KERNEL_SCORE = 1, KERNEL_FILTER = 2, KERNEL_FINAL =
 // Full (dense) attention: rows per chunk block, and the chunk count for a length.
 constexpr int kDenseRows = 1024;
 constexpr int kDenseThreads = 512;
+constexpr int kMergeThreads = 1024;  // dense merge block: one per query head
 
 // Fills *k for kernel `which` of a step in a.mode (retopk_kernels.hip).
 // dtype: 0 = f32, 1 = bf16.

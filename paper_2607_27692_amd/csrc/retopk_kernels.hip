@@ -1504,9 +1504,9 @@ __global__ __launch_bounds__(kDenseThreads, 4) void k_dense(StepArgs a, Ws w)
 // with M the largest chunk maximum.  The chunks are spread over the waves, the
 // head dimension over the lanes, with several chunks' loads in flight.
 template <int D>
-__global__ __launch_bounds__(256) void k_dense_merge(StepArgs a, Ws w)
+__global__ __launch_bounds__(kMergeThreads) void k_dense_merge(StepArgs a, Ws w)
 {
-    constexpr int NT = 256, NW = NT / 64, EPL = D / 64, U = 4;
+    constexpr int NT = kMergeThreads, NW = NT / 64, EPL = D / 64, U = 8;
     static_assert(D % 64 == 0, "whole elements per lane");
     __shared__ float s_red[NW];
     __shared__ float s_o[NW][D];
@@ -1650,7 +1650,7 @@ void describe_kernel(int which, int dtype, const StepArgs &a, const Geometry &ge
         return d64 ? dense_g<float, 64>(a, k) : dense_g<float, 128>(a, k);
     case KERNEL_DENSE_MERGE:
         *k = KernelDesc{d64 ? (const void *)&k_dense_merge<64> : (const void *)&k_dense_merge<128>,
-                        dim3((unsigned)(a.B * a.Hq)), dim3(256), 0u, 2};
+                        dim3((unsigned)(a.B * a.Hq)), dim3(kMergeThreads), 0u, 2};
         return;
     default:
         if (bf) return d64 ? final_desc<uint16_t, 64>(a, k) : final_desc<uint16_t, 128>(a, k);
