@@ -130,6 +130,19 @@ def main():
     h.close()
     log("[bench] warm-up done")
 
+    # ---- prefill initialisation (Sec. 3.3), timed once on its own handle -------
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    h = R.Handle(**cfg)
+    h.profile(True)
+    h.prefill_init(q_tail, w.cache_cap, k, v, w.prompt_len)
+    torch.cuda.synchronize()
+    pf_ms = (time.perf_counter() - t0) * 1e3
+    pf_prof = h.profile_read()
+    h.profile(False)
+    h.close()
+    log(f"[bench] prefill initialisation: {pf_ms:.2f} ms")
+
     def timed(run, profile):
         """One pass over the timed steps on a fresh handle (prefill untimed)."""
         handle = fresh_handle()
@@ -255,6 +268,16 @@ def main():
                      "avg_launch_us": round(tot_ms / launches * 1e3, 2),
                      "bytes_per_launch": round(fb / launches)}
 
+    # Prefill: 2 d flops per (position, head, causal key) on the matrix cores.
+    n_pf = w.cache_cap
+    pf_flops = 2.0 * d * BH * sum(w.prompt_len - n_pf + u + 1 for u in range(n_pf))
+    pf_score = pf_prof.get("prefill_score", (0, 0.0))
+    prefill = {"ms": round(pf_ms, 3), "positions": n_pf,
+               "kernels": {n: {"launches": l, "ms": round(ms, 3)} for n, (l, ms) in
+                           pf_prof.items() if l},
+               "prefill_score_tflops": round(pf_flops / (pf_score[1] * 1e-3) / 1e12, 1)
+               if pf_score[0] else None}
+
     # ---- CPU baseline: the oracle on a bounded sample ------------------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -303,6 +326,7 @@ def main():
         "roofline": roof,
         "exact_roofline": exact_roof,
         "full_attention_roofline": full_roof,
+        "prefill_init": prefill,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
@@ -625,6 +649,7 @@ SYMBOLS = {  # kernel symbol prefix -> name used by the library's own profiling
     "void retopk::k_final<": "retopk_final",
     "void retopk::k_dense<": "dense_chunk",
     "void retopk::k_dense_merge<": "dense_merge",
+    "void retopk::k_pf_score<": "prefill_score",
 }
 
 
@@ -643,8 +668,9 @@ def _read_csv(path):
 
 def _passes(names, w, steps, warmup):
     """Splits the library's dispatches (in dispatch order) into the bench's
-    passes.  Every pass starts on a fresh handle whose prefill issues one
-    scan, filter, final triple per prompt-tail query; a decode step that selects
+    passes.  Every pass starts on a fresh handle whose prefill issues a
+    prefill_score, filter, final triple per launch of prompt-tail positions (a
+    scan, filter, final triple per position for f32); a decode step that selects
     issues sim, score, filter, final, any other step or an Exact Top-K step
     scan, filter, final, and a full-attention step dense_chunk, dense_merge.
     The warm-up runs one step of each kind per warm-up step.  Returns
@@ -656,10 +682,15 @@ def _passes(names, w, steps, warmup):
              "retopk_scan": ["retopk_scan", "retopk_filter", "retopk_final"],
              "dense_chunk": ["dense_chunk", "dense_merge"]}
     out, i = [], 0
+    pf = ["prefill_score", "retopk_filter", "retopk_final"]
     for label, n_units in plan:
-        for _ in range(w.cache_cap):
-            assert names[i:i + 3] == units["retopk_scan"], f"unexpected prefill dispatches at {i}"
-            i += 3
+        if names[i] == "prefill_score":
+            while names[i:i + 3] == pf:
+                i += 3
+        else:
+            for _ in range(w.cache_cap):
+                assert names[i:i + 3] == units["retopk_scan"], f"unexpected prefill at {i}"
+                i += 3
         start = i
         for _ in range(n_units):
             unit = units.get(names[i])

@@ -118,7 +118,12 @@ retopk_status retopk_destroy(retopk_handle h);
  * at positions prefill_len-n .. prefill_len-1; query u is given its Exact Top-K
  * support over its causal prefix (len = prefill_len-n+u+1) and inserted, in
  * order.  Requires n >= 0 and n <= prefill_len <= max_len.  Does not advance the
- * decode-step counter. */
+ * decode-step counter.  Queries whose slot a later one overwrites (n > C) only
+ * advance the insertion count.  bf16 handles score many positions of every head
+ * per launch on the matrix cores (kernel id 7) with up to 2 GiB of temporary
+ * device memory, and return after the stream has finished that work; when the
+ * memory is not available, and for f32, the queries run one position at a time
+ * through the decode step's exact path, asynchronously. */
 retopk_status retopk_prefill_init(retopk_handle h, const void *q_tail, int32_t n,
                                   const void *k, const void *v, int64_t prefill_len,
                                   void *stream);
@@ -178,7 +183,9 @@ retopk_status retopk_set_state(retopk_handle h, const float *qbar, const int32_t
  *   3 retopk_filter  threshold bucket and survivor compaction
  *   4 retopk_final   exact Top-K, Softmax-V, cache insert
  *   5 dense_chunk    full_attention: per-chunk softmax and value sums
- *   6 dense_merge    full_attention: merge of the chunks */
+ *   6 dense_merge    full_attention: merge of the chunks
+ *   7 prefill_score  bf16 prefill: scores of many prompt-tail positions of every
+ *                    head (matrix cores); retopk_filter and retopk_final select */
 retopk_status retopk_profile(retopk_handle h, int32_t enable);
 retopk_status retopk_profile_read(retopk_handle h, int32_t n_kernels, uint64_t *launches,
                                   double *total_ms);

@@ -17,15 +17,18 @@ using namespace retopk;
 namespace {
 
 constexpr int kProfileMaxLaunches = 65536;
-constexpr int kNumKernels = 7;
+constexpr int kNumKernels = 8;
+// Temporary device memory one batched prefill launch sequence may use (scores,
+// survivors and histograms of U positions of every head).
+constexpr size_t kPfWorkspaceBytes = (size_t)2 << 30;
 // retopk_score is the scoring kernel of a decode step that selects (candidate
 // blocks beside the scans of fallback heads); retopk_scan is the same kernel
 // built for steps where every head takes the full-history scan.
 const char *const kKernelNames[kNumKernels] = {"retopk_sim", "retopk_score", "retopk_scan",
                                                "retopk_filter", "retopk_final", "dense_chunk",
-                                               "dense_merge"};
+                                               "dense_merge", "prefill_score"};
 enum { KID_SIM = 0, KID_SCORE = 1, KID_SCAN = 2, KID_FILTER = 3, KID_FINAL = 4, KID_DENSE = 5,
-       KID_DENSE_MERGE = 6 };
+       KID_DENSE_MERGE = 6, KID_PF_SCORE = 7 };
 
 }  // namespace
 
@@ -119,6 +122,7 @@ StepArgs base_args(const retopk_handle_s *h)
     a.retrieval = c.retrieval;
     a.inv_sqrt_d = h->inv_sqrt_d;
     a.q_head_stride = c.head_dim;
+    a.U = 1;
     return a;
 }
 
@@ -205,6 +209,85 @@ retopk_status run_step(retopk_handle h, const StepArgs &a, int mode, hipStream_t
         if (st != RETOPK_OK) return st;
     }
     return RETOPK_OK;
+}
+
+// Batched prefill initialisation (bf16): positions u_first .. n-1 of q_tail in
+// launches of U positions each, every launch scoring its U x B x Hq virtual
+// heads on the matrix cores (k_pf_score) and selecting and inserting them with
+// k_filter and k_final, on temporary workspaces.  Returns RETOPK_ERR_OOM, having
+// launched nothing, when the workspaces cannot be allocated.
+retopk_status prefill_batched(retopk_handle h, const char *q_tail, int32_t n, int32_t u_first,
+                              const void *k, const void *v, int64_t prefill_len, hipStream_t s)
+{
+    const retopk_config &c = h->cfg;
+    const int64_t BH = heads_of(c);
+    StepArgs a = base_args(h);
+    const int64_t NR = a.n_regions, RS = a.row_stride;
+    const size_t per_u = (size_t)BH * ((size_t)RS * (8 + 4) + (size_t)NR * 4 + (size_t)kHistBins * 4);
+    const int32_t n_eff = n - u_first;
+    int64_t U = (int64_t)(kPfWorkspaceBytes / per_u);
+    // whole query tiles where the budget allows: U a multiple of kPfCols / gcd(G, kPfCols)
+    int gcd = h->G, m = kPfCols;
+    while (m) {
+        const int r = gcd % m;
+        gcd = m;
+        m = r;
+    }
+    const int64_t step = kPfCols / gcd;
+    if (U >= step) U -= U % step;
+    U = U < 1 ? 1 : (U > n_eff ? n_eff : U);
+    void *mem = nullptr;
+    if (hipMalloc(&mem, per_u * (size_t)U + 1024) != hipSuccess) {
+        (void)hipGetLastError();
+        return RETOPK_ERR_OOM;
+    }
+    Ws w = h->w;
+    char *p = (char *)mem;
+    w.surv = (uint64_t *)p;
+    p += (size_t)U * BH * RS * 8;
+    w.scores = (float *)p;
+    p += (size_t)U * BH * RS * 4;
+    w.hist = (uint32_t *)p;
+    p += (size_t)U * BH * kHistBins * 4;
+    w.surv_cnt = (uint32_t *)p;
+    retopk_status st = RETOPK_OK;
+    if (hipMemsetAsync(w.hist, 0, (size_t)U * BH * kHistBins * 4, s) != hipSuccess) st = fail(h);
+    const size_t es = elem_size(c);
+    for (int32_t u0 = u_first; u0 < n && st == RETOPK_OK; u0 += (int32_t)U) {
+        const int32_t Uc = (int32_t)(n - u0 < U ? n - u0 : U);
+        StepArgs b = a;
+        b.mode = MODE_PREFILL;
+        b.U = Uc;
+        b.q = q_tail + (size_t)u0 * c.head_dim * es;
+        b.q_head_stride = (int64_t)n * c.head_dim;
+        b.k = k;
+        b.v = v;
+        b.len = prefill_len - n + u0 + 1;
+        b.out = nullptr;
+        b.sel = nullptr;
+        b.n_ins = h->n_ins;
+        b.insert_slot = (int32_t)(h->n_ins % c.cache_cap);
+        b.do_insert = 1;
+        const int64_t len_max = b.len + Uc - 1;
+        Geometry geo{};
+        geo.filter_blocks_per_head = (int)ceil_div(len_max, kFilterRows);
+        geo.pf_qtiles = (int)ceil_div((int64_t)h->G * Uc, kPfCols);
+        geo.pf_kchunks = (int)ceil_div(len_max, kPfKeys);
+        geo.pf_pairs = c.batch * c.n_kv_heads * geo.pf_kchunks;
+        void *args[3] = {&b, &w, &geo};
+        const int kinds[3] = {KERNEL_PF_SCORE, KERNEL_FILTER, KERNEL_FINAL};
+        const int kids[3] = {KID_PF_SCORE, KID_FILTER, KID_FINAL};
+        for (int i = 0; i < 3 && st == RETOPK_OK; ++i) {
+            KernelDesc d;
+            describe_kernel(kinds[i], c.dtype, b, geo, &d);
+            st = launch_desc(h, d, kids[i], args, s);
+        }
+        h->n_ins += Uc;
+    }
+    // the workspaces are released once the launches that use them are done
+    if (hipStreamSynchronize(s) != hipSuccess && st == RETOPK_OK) st = fail(h);
+    (void)hipFree(mem);
+    return st;
 }
 
 retopk_status sync_last(retopk_handle h)
@@ -383,8 +466,18 @@ retopk_status retopk_prefill_init(retopk_handle h, const void *q_tail, int32_t n
     if (c.cache_cap == 0 || n == 0) return RETOPK_OK;
     hipStream_t s = (hipStream_t)stream;
     if (hipSetDevice(h->device) != hipSuccess) return fail(h);
+    // Positions whose slot a later prompt-tail query overwrites (n > C) only
+    // advance the insertion count.
+    const int32_t u_first = n > c.cache_cap ? n - c.cache_cap : 0;
+    h->n_ins += u_first;
+    h->last_stream = s;
+    if (c.dtype == RETOPK_BF16 && n - u_first > 1) {
+        const retopk_status st = prefill_batched(h, (const char *)q_tail, n, u_first, k, v,
+                                                 prefill_len, s);
+        if (st != RETOPK_ERR_OOM) return st;
+    }
     const size_t es = elem_size(c);
-    for (int32_t u = 0; u < n; ++u) {
+    for (int32_t u = u_first; u < n; ++u) {
         StepArgs a = base_args(h);
         a.mode = MODE_PREFILL;
         a.q = (const char *)q_tail + (size_t)u * c.head_dim * es;

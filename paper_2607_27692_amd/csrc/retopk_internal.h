@@ -32,6 +32,14 @@ constexpr int kScanBlocksSelect = 256;  // k_score scan blocks in MODE_SELECT
 constexpr int kScanBlocksExact = 2048;  // k_score scan blocks when every head is exact
 constexpr int64_t kMaxLen = (int64_t)kMaxRegions * kFilterRows;
 
+// Batched prefill initialisation (bf16): k_pf_score blocks take kPfCols virtual
+// queries (one MFMA column each) against kPfKeys keys of one KV group.
+constexpr int kPfThreads = 512;
+constexpr int kPfCols = 32;
+constexpr int kPfKeys = 4096;
+constexpr int kPfTiles = 2;           // 16-key tiles per wave per iteration
+constexpr int kPfHistStride = kHistBins / 2 + 1;   // padded LDS histogram row (16-bit counts)
+
 // Step modes.  SELECT runs the per-head path rule on the device; the others take
 // the exact path for every head.
 enum Mode : int {
@@ -92,7 +100,11 @@ struct StepArgs {
     int64_t q_head_stride;
     const void *k;
     const void *v;
-    int64_t len;
+    int64_t len;               // with U > 1: the length of position 0 of the launch
+    int U;                     // query positions per launch: 1, or more in the batched
+                               // prefill, where virtual head vh = u * B * Hq + bh holds
+                               // position u (length len + u, q at + u * d, slot
+                               // insert_slot + u) in the workspaces
     float *out;                // nullable in MODE_PREFILL
     int32_t *sel;              // nullable
     int64_t n_ins;             // insertions before this step
@@ -111,6 +123,9 @@ struct Geometry {
     int scan_blocks;           // scan blocks of k_score (they split the scanned rows)
     int cand_blocks;           // B * Hq * kCandRanges in MODE_SELECT, else 0
     int filter_blocks_per_head;
+    // batched prefill (k_pf_score): (KV group, key chunk) pairs, query tiles of
+    // kPfCols virtual queries, key chunks of kPfKeys keys per group
+    int pf_pairs, pf_qtiles, pf_kchunks;
 };
 
 // One kernel of a step, ready to launch (hipLaunchKernel) or to put in a graph
@@ -124,7 +139,7 @@ struct KernelDesc {
     int nargs;
 };
 enum : int { KERNEL_SIM = 0, KERNEL_SCORE = 1, KERNEL_FILTER = 2, KERNEL_FINAL = 3,
-              KERNEL_DENSE = 4, KERNEL_DENSE_MERGE = 5 };
+              KERNEL_DENSE = 4, KERNEL_DENSE_MERGE = 5, KERNEL_PF_SCORE = 6 };
 
 // Full (dense) attention: rows per chunk block, and the chunk count for a length.
 constexpr int kDenseRows = 1024;

@@ -844,15 +844,16 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
     __shared__ uint32_t s_red[NT / 64];
     __shared__ uint32_t s_bstar;
     const int tid = threadIdx.x;
-    const int bh = blockIdx.x / geo.filter_blocks_per_head;
+    const int vh = blockIdx.x / geo.filter_blocks_per_head;   // the head (a.U == 1)
     const int f = blockIdx.x % geo.filter_blocks_per_head;
-    if (a.mode == MODE_SELECT && w.path[bh] == PATH_REUSE) return;
+    const int64_t len = a.U > 1 ? a.len + vh / (a.B * a.Hq) : a.len;
+    if (a.mode == MODE_SELECT && w.path[vh] == PATH_REUSE) return;
 
     // This block's scores and the head's histogram in one round trip.
     const int64_t i0 = (int64_t)f * kFilterRows + (int64_t)tid * EPT;
-    const float4 *src = (const float4 *)(w.scores + (int64_t)bh * a.row_stride + i0);
+    const float4 *src = (const float4 *)(w.scores + (int64_t)vh * a.row_stride + i0);
     const float4 v0 = src[0], v1 = src[1];
-    const uint32_t *hist = w.hist + (int64_t)bh * kHistBins;
+    const uint32_t *hist = w.hist + (int64_t)vh * kHistBins;
     uint32_t c[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) c[j] = hist[kHistBins - 1 - 4 * tid - j];
@@ -860,7 +861,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
     // The bin b* that holds the kn-th largest score: the largest b with
     // count(bins >= b) >= kn.  Thread t holds bins 2047-4t .. 2044-4t.
     {
-        const uint32_t kn = (uint32_t)(a.K < a.len ? a.K : a.len);
+        const uint32_t kn = (uint32_t)(a.K < len ? a.K : len);
         uint32_t all;
         uint32_t above = block_excl_scan<NT>(c[0] + c[1] + c[2] + c[3], s_red, &all);
 #pragma unroll
@@ -875,17 +876,17 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
     uint32_t keep = 0, n = 0;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
-        const bool k = i0 + e < a.len && ord_key(sv[e]) >= kmin;
+        const bool k = i0 + e < len && ord_key(sv[e]) >= kmin;
         keep |= (uint32_t)k << e;
         n += k ? 1u : 0u;
     }
     uint32_t total;
     uint32_t pos = block_excl_scan<NT>(n, s_red, &total);
-    uint64_t *dst = w.surv + (int64_t)bh * a.row_stride + (int64_t)f * kFilterRows;
+    uint64_t *dst = w.surv + (int64_t)vh * a.row_stride + (int64_t)f * kFilterRows;
 #pragma unroll
     for (int e = 0; e < EPT; ++e)
         if ((keep >> e) & 1u) dst[pos++] = rank_of(sv[e], (uint32_t)(i0 + e));
-    if (tid == 0) w.surv_cnt[(int64_t)bh * a.n_regions + f] = total;
+    if (tid == 0) w.surv_cnt[(int64_t)vh * a.n_regions + f] = total;
 }
 
 // ---------------------------------------------------------------------------
@@ -1062,7 +1063,9 @@ __device__ bool value_threshold(const uint64_t *ent, int n, int K, FinalSmem<D, 
     return true;
 }
 
-template <typename T, int D>
+// kMulti: built for launches of several query positions (a.U > 1, the batched
+// prefill); the decode-step build keeps u = 0 out of its code.
+template <typename T, int D, bool kMulti>
 __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
 {
     constexpr int NT = kFinalThreads;
@@ -1077,9 +1080,15 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     static_assert(kMaxRegions % NT == 0 && kCandRanges <= NT, "region ownership");
     __shared__ FinalSmem<D, NT> sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bh = blockIdx.x / kFinalSlices, slice = blockIdx.x % kFinalSlices;
+    const int vh = blockIdx.x / kFinalSlices, slice = blockIdx.x % kFinalSlices;
     const bool writes_out = a.out != nullptr && a.mode != MODE_PREFILL;
     if (slice != 0 && !writes_out) return;
+    // Virtual head vh = u * B * Hq + bh: query position u of head bh (u = 0 unless
+    // a batched prefill launch); the workspaces are indexed by vh, the cache, q
+    // and the outputs by bh.
+    const int u = kMulti ? vh / (a.B * a.Hq) : 0;
+    const int bh = kMulti ? vh - u * a.B * a.Hq : vh;
+    const int64_t len = kMulti ? a.len + u : a.len;
 
     if (slice == 0 && (a.mode == MODE_REFRESH || a.mode == MODE_COLD)) {
         const int8_t code = a.mode == MODE_REFRESH ? PATH_REFRESH : PATH_COLD;
@@ -1096,14 +1105,14 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     // count is known only afterwards).
     const bool sel_mode = a.mode == MODE_SELECT;
     const bool reuse = sel_mode && w.path[bh] == PATH_REUSE;
-    const int nreg_s = (int)((a.len + kFilterRows - 1) / kFilterRows);
+    const int nreg_s = (int)((len + kFilterRows - 1) / kFilterRows);
     const int rpt = (nreg_s + NT - 1) / NT;
     uint32_t scnt[kRegPerThread];
 #pragma unroll
     for (int u = 0; u < kRegPerThread; ++u) {
         const int r = tid * rpt + u;
         const bool ok = u < rpt && r < nreg_s;
-        const uint32_t x = w.surv_cnt[(int64_t)bh * a.n_regions + (ok ? r : 0)];
+        const uint32_t x = w.surv_cnt[(int64_t)vh * a.n_regions + (ok ? r : 0)];
         scnt[u] = ok ? x : 0u;
     }
     const uint32_t ccnt_l = w.cand_cnt[(int64_t)bh * kCandRanges + (tid < kCandRanges ? tid : 0)];
@@ -1115,7 +1124,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
         rg.stride = a.cand_cap;
         rg.nreg = kCandRanges;
     } else {
-        rg.base = w.surv + (int64_t)bh * a.row_stride;
+        rg.base = w.surv + (int64_t)vh * a.row_stride;
         rg.stride = kFilterRows;
         rg.nreg = nreg_s;
     }
@@ -1314,11 +1323,11 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
             a.sel[(int64_t)bh * a.K + t] = t < kn ? (int32_t)(sm.sel[t] >> 32) : -1;
     if (a.do_insert) {
         // Sec. 3.4: insert (q_bar, support) after either path.
-        const int64_t e = (int64_t)bh * a.M + a.insert_slot;
+        const int64_t e = (int64_t)bh * a.M + (kMulti ? (a.insert_slot + u) % a.M : a.insert_slot);
         if (a.mode == MODE_SELECT) {
             for (int t = tid; t < D; t += NT) w.qbar[e * D + t] = w.qbar_cur[(int64_t)bh * D + t];
         } else {
-            const T *q = (const T *)a.q + (int64_t)bh * a.q_head_stride;
+            const T *q = (const T *)a.q + (int64_t)bh * a.q_head_stride + (int64_t)u * D;
             block_qbar<T, D, NT>(q, sm.qbar, sm.red64);
             for (int t = tid; t < D; t += NT) w.qbar[e * D + t] = sm.qbar[t];
         }
@@ -1333,12 +1342,152 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
         }
     } else {
         // leave the histogram zeroed for the next launch
-        for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)bh * kHistBins + i] = 0u;
+        for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)vh * kHistBins + i] = 0u;
     }
     if (a.dbg_ncand && tid == 0) a.dbg_ncand[bh] = reuse ? rg.n : 0;
     if (a.dbg_cand)
         for (int j = tid; j < a.cand_cap; j += NT)
             a.dbg_cand[(int64_t)bh * a.cand_cap + j] = (reuse && j < rg.n) ? (int32_t)rank_index(rg.get(j)) : -1;
+}
+
+// ---------------------------------------------------------------------------
+// Batched prefill initialisation (Sec. 3.3): the prompt-tail queries of U
+// positions at once, each against its causal prefix
+// ---------------------------------------------------------------------------
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// k_pf_score: the scores of Eq. 4 for U positions x G heads of a KV group (the
+// group's "virtual queries", vq = u * G + j) as a matrix product on the matrix
+// cores.  Block (pair, tile) takes keys [kc * kPfKeys, ...) of KV group grp for
+// the kPfCols virtual queries of query tile `tile`, in column tiles of 16, with
+// v_mfma_f32_16x16x32_bf16: the A operand is 16 key rows x 32 dims, B is 32 dims
+// x 16 queries, and lane l supplies key row (and query) l % 16 for dims
+// 8 (l / 16) .. + 7 of each 32-dim step and receives keys 4 (l / 16) .. + 3 of
+// query l % 16.  Each key tile loaded serves every column tile.  Keys at or past
+// a query's causal length are left out of its histogram (LDS, two 16-bit counts
+// per word, added to the global histogram at the end); every score is stored to
+// the virtual head's score row, those past the causal length included (no later
+// stage reads them), so that each wave issues the same stores every iteration
+// and its key loads, two iterations ahead, never wait for them.  The blocks of
+// one (group, key chunk) pair share blockIdx % 8, so they run on one XCD and
+// read the chunk's keys through one L2.
+template <int D>
+__global__ __launch_bounds__(kPfThreads) void k_pf_score(StepArgs a, Ws w, Geometry geo)
+{
+    constexpr int NT = kPfThreads, NW = NT / 64, TW = kPfTiles, KS = D / 32;
+    constexpr int CT = kPfCols / 16;
+    constexpr int ROWS = NW * TW * 16;
+    constexpr int ITERS = kPfKeys / ROWS;
+    // A chunk's stores stay inside its score row: chunks end on filter-region
+    // boundaries, and score rows are whole regions long.
+    static_assert(D % 32 == 0 && kPfKeys % (2 * ROWS) == 0 && kFilterRows % kPfKeys == 0 &&
+                  kPfCols % 16 == 0, "tile geometry");
+    static_assert(kPfKeys < 65536 && kPfHistStride * 2 > kHistBins, "16-bit bin counts");
+    __shared__ uint32_t s_hist[kPfCols * kPfHistStride];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, kq = lane >> 4;
+    const int j = (int)blockIdx.x;
+    const int pair = (j & 7) + 8 * (j / (8 * geo.pf_qtiles));
+    const int tile = (j >> 3) % geo.pf_qtiles;
+    if (pair >= geo.pf_pairs) return;
+    const int grp = pair / geo.pf_kchunks, kc = pair % geo.pf_kchunks;
+    const int b = grp / a.Hkv, g = grp % a.Hkv;
+    const int BH = a.B * a.Hq;
+    const int nvq = a.G * a.U;
+    // rows of this block: the chunk, cut at the longest causal length of the tile
+    const int last_vq = (tile + 1) * kPfCols - 1 < nvq - 1 ? (tile + 1) * kPfCols - 1 : nvq - 1;
+    const int64_t tlen = a.len + last_vq / a.G;
+    const int64_t k0 = (int64_t)kc * kPfKeys;
+    const int64_t k1 = k0 + kPfKeys < tlen ? k0 + kPfKeys : tlen;
+    if (k0 >= k1) return;
+
+    // This lane's virtual query in each column tile; columns past the last one
+    // repeat it (same query, same score row, same values stored) and count nothing.
+    bf16x8_t qb[CT][KS];
+    float *srow[CT];
+    int64_t cend[CT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+        const int vq = tile * kPfCols + ct * 16 + col;
+        const bool cvalid = vq < nvq;
+        const int vqe = cvalid ? vq : nvq - 1;
+        const int u = vqe / a.G;
+        const int bh = b * a.Hq + g * a.G + vqe % a.G;
+        const uint4 *qr = (const uint4 *)((const uint16_t *)a.q + (int64_t)bh * a.q_head_stride +
+                                          (int64_t)u * D);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qb[ct][ks] = __builtin_bit_cast(bf16x8_t, qr[ks * 4 + kq]);
+        srow[ct] = w.scores + ((int64_t)u * BH + bh) * a.row_stride;
+        const int64_t clen = cvalid ? a.len + u : 0;
+        cend[ct] = clen < k1 ? clen : k1;           // rows counted for this query
+    }
+    const uint16_t *kbase = (const uint16_t *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
+    auto load = [&](uint4 (&kv)[TW][KS], int64_t base) {
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            const int64_t r = base + (wave * TW + t) * 16 + col;
+            const uint4 *rp = (const uint4 *)(kbase + (r < k1 ? r : k0) * D);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) kv[t][ks] = rp[ks * 4 + kq];
+        }
+    };
+    // One iteration: the scores of ROWS keys from kv, the loads of the keys two
+    // iterations on into kv, the stores and the histogram counts.
+    auto step = [&](uint4 (&kv)[TW][KS], int64_t base) {
+        f32x4_t acc[CT][TW];
+#pragma unroll
+        for (int t = 0; t < TW; ++t)
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                acc[ct][t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+                    acc[ct][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8_t, kv[t][ks]), qb[ct][ks], acc[ct][t], 0, 0, 0);
+            }
+        load(kv, base + 2 * ROWS);   // past k1 the clamped rows are re-read, never used
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+            uint32_t *hrow = s_hist + (ct * 16 + col) * kPfHistStride;
+#pragma unroll
+            for (int t = 0; t < TW; ++t) {
+                const int64_t r4 = base + (wave * TW + t) * 16 + 4 * kq;
+                const float sc[4] = {acc[ct][t][0] * a.inv_sqrt_d, acc[ct][t][1] * a.inv_sqrt_d,
+                                     acc[ct][t][2] * a.inv_sqrt_d, acc[ct][t][3] * a.inv_sqrt_d};
+                *(float4 *)(srow[ct] + r4) = make_float4(sc[0], sc[1], sc[2], sc[3]);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (r4 + i < cend[ct]) {
+                        const uint32_t bin = ord_key(sc[i]) >> kHistShift;
+                        atomicAdd(&hrow[bin >> 1], 1u << ((bin & 1u) << 4));
+                    }
+                }
+            }
+        }
+    };
+    uint4 kva[TW][KS], kvb[TW][KS];
+    load(kva, k0);   // the first key rows are in flight while the histogram is cleared
+    load(kvb, k0 + ROWS);
+    for (int i = tid; i < kPfCols * kPfHistStride; i += NT) s_hist[i] = 0u;
+    __syncthreads();
+    // A fixed trip count: rows past k1 (the chunk cut short by the causal limit)
+    // are computed from clamped loads and stored where nothing reads them.
+    for (int it = 0; it < ITERS; it += 2) {
+        step(kva, k0 + (int64_t)it * ROWS);
+        step(kvb, k0 + (int64_t)(it + 1) * ROWS);
+    }
+    __syncthreads();
+    for (int i = tid; i < kPfCols * kHistBins; i += NT) {
+        const int c = i / kHistBins, bin = i % kHistBins;
+        const int cvq = tile * kPfCols + c;
+        const uint32_t n = (s_hist[c * kPfHistStride + (bin >> 1)] >> ((bin & 1) << 4)) & 0xFFFFu;
+        if (n && cvq < nvq) {
+            const int cbh = b * a.Hq + g * a.G + cvq % a.G;
+            atomicAdd(&w.hist[((int64_t)(cvq / a.G) * BH + cbh) * kHistBins + bin], n);
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1501,67 +1650,67 @@ __global__ __launch_bounds__(kDenseThreads, 4) void k_dense(StepArgs a, Ws w)
 }
 
 // k_dense_merge: one block per head; out = sum_c e^(m_c - M) o_c / sum_c e^(m_c - M) l_c
-// with M the largest chunk maximum.  The chunks are spread over the waves, the
-// head dimension over the lanes, with several chunks' loads in flight.
+// with M the largest chunk maximum.  Each wave folds its share of the chunks
+// into a running (maximum, sum, output) with rescaling, so every chunk is read
+// once, all in one round trip; the waves' partials are then combined the same way.
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void k_dense_merge(StepArgs a, Ws w)
 {
     constexpr int NT = kMergeThreads, NW = NT / 64, EPL = D / 64, U = 8;
     static_assert(D % 64 == 0, "whole elements per lane");
-    __shared__ float s_red[NW];
+    __shared__ float s_m[NW], s_l[NW];
     __shared__ float s_o[NW][D];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, bh = blockIdx.x;
     const int nch = (int)((a.len + kDenseRows - 1) / kDenseRows);
     const float *part = w.dense_part + (int64_t)bh * a.n_dense * (D + 2);
-    // M, then L = sum_c e^(m_c - M) l_c
-    float mx = -INFINITY;
-    for (int c = tid; c < nch; c += NT) mx = fmaxf(mx, part[(int64_t)c * (D + 2) + D]);
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-    if (lane == 0) s_red[wave] = mx;
-    __syncthreads();
-    float M = s_red[0];
-#pragma unroll
-    for (int i = 1; i < NW; ++i) M = fmaxf(M, s_red[i]);
-    __syncthreads();
-    float l = 0.0f;
-    for (int c = tid; c < nch; c += NT) {
-        const float *pc = part + (int64_t)c * (D + 2);
-        l += expf(pc[D] - M) * pc[D + 1];
-    }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o);
-    if (lane == 0) s_red[wave] = l;
-    // o: chunk c by wave c % NW, EPL consecutive elements per lane
-    float acc[EPL];
+    float mw = -INFINITY, lw = 0.0f, acc[EPL];
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[e] = 0.0f;
     for (int c0 = wave; c0 < nch; c0 += NW * U) {
-        float mv[U], ov[U][EPL];
+        float mv[U], lv[U], ov[U][EPL];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int c = c0 + u * NW < nch ? c0 + u * NW : c0;
             const float *pc = part + (int64_t)c * (D + 2);
             mv[u] = pc[D];
+            lv[u] = pc[D + 1];
 #pragma unroll
             for (int e = 0; e < EPL; ++e) ov[u][e] = pc[lane * EPL + e];
         }
+        float mn = mw;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c0 + u * NW < nch) mn = fmaxf(mn, mv[u]);
+        const float f0 = mw == -INFINITY ? 0.0f : expf(mw - mn);
+        lw *= f0;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[e] *= f0;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const float f = c0 + u * NW < nch ? expf(mv[u] - M) : 0.0f;
+            const float f = c0 + u * NW < nch ? expf(mv[u] - mn) : 0.0f;
+            lw += f * lv[u];
 #pragma unroll
             for (int e = 0; e < EPL; ++e) acc[e] += f * ov[u][e];
         }
+        mw = mn;
+    }
+    if (lane == 0) {
+        s_m[wave] = mw;
+        s_l[wave] = lw;
     }
 #pragma unroll
     for (int e = 0; e < EPL; ++e) s_o[wave][lane * EPL + e] = acc[e];
     __syncthreads();
     if (tid < D) {
+        float M = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) M = fmaxf(M, s_m[i]);
         float L = 0.0f, o = 0.0f;
 #pragma unroll
         for (int i = 0; i < NW; ++i) {
-            L += s_red[i];
-            o += s_o[i][tid];
+            const float f = s_m[i] == -INFINITY ? 0.0f : expf(s_m[i] - M);
+            L += f * s_l[i];
+            o += f * s_o[i][tid];
         }
         a.out[(int64_t)bh * D + tid] = o / L;
     }
@@ -1602,7 +1751,8 @@ static void score_desc(const StepArgs &a, const Geometry &geo, KernelDesc *k)
 template <typename T, int D>
 static void final_desc(const StepArgs &a, KernelDesc *k)
 {
-    *k = KernelDesc{(const void *)&k_final<T, D>, dim3((unsigned)(a.B * a.Hq * kFinalSlices)),
+    *k = KernelDesc{a.U > 1 ? (const void *)&k_final<T, D, true> : (const void *)&k_final<T, D, false>,
+                    dim3((unsigned)(a.B * a.Hq * a.U * kFinalSlices)),
                     dim3(kFinalThreads), 0u, 2};
 }
 
@@ -1642,8 +1792,14 @@ void describe_kernel(int which, int dtype, const StepArgs &a, const Geometry &ge
         if (bf) return d64 ? score_g<uint16_t, 64>(a, geo, k) : score_g<uint16_t, 128>(a, geo, k);
         return d64 ? score_g<float, 64>(a, geo, k) : score_g<float, 128>(a, geo, k);
     case KERNEL_FILTER:
-        *k = KernelDesc{(const void *)&k_filter, dim3((unsigned)(a.B * a.Hq * geo.filter_blocks_per_head)),
+        *k = KernelDesc{(const void *)&k_filter,
+                        dim3((unsigned)(a.B * a.Hq * a.U * geo.filter_blocks_per_head)),
                         dim3(kScoreThreads), 0u, 3};
+        return;
+    case KERNEL_PF_SCORE:   // bf16 only
+        *k = KernelDesc{d64 ? (const void *)&k_pf_score<64> : (const void *)&k_pf_score<128>,
+                        dim3((unsigned)(((geo.pf_pairs + 7) / 8) * 8 * geo.pf_qtiles)),
+                        dim3(kPfThreads), 0u, 3};
         return;
     case KERNEL_DENSE:
         if (bf) return d64 ? dense_g<uint16_t, 64>(a, k) : dense_g<uint16_t, 128>(a, k);

@@ -37,10 +37,10 @@ def test_every_declared_symbol_is_exported(lib):
 def test_status_strings(lib):
     for code in (0, -1, -2, -3, -4, -5):
         assert R.retopk_status_string(code) == R.STATUS[code]
-    assert [R.retopk_kernel_name(i) for i in range(7)] == [
+    assert [R.retopk_kernel_name(i) for i in range(8)] == [
         "retopk_sim", "retopk_score", "retopk_scan", "retopk_filter", "retopk_final",
-        "dense_chunk", "dense_merge"]
-    assert R.retopk_kernel_name(7) is None and R.retopk_kernel_name(-1) is None
+        "dense_chunk", "dense_merge", "prefill_score"]
+    assert R.retopk_kernel_name(8) is None and R.retopk_kernel_name(-1) is None
 
 
 def _cfg(**kw):
