@@ -673,9 +673,11 @@ def _passes(names, w, steps, warmup):
     scan, filter, final triple per position for f32); a decode step that selects
     issues sim, score, filter, final, any other step or an Exact Top-K step
     scan, filter, final, and a full-attention step dense_chunk, dense_merge.
-    The warm-up runs one step of each kind per warm-up step.  Returns
-    (label, first, end) positions of each pass's step dispatches."""
-    plan = [("warm-up", 3 * min(warmup, w.steps)), ("retopk timed", steps),
+    The warm-up runs one step of each kind per warm-up step, then one handle
+    runs the timed prefill alone.  Returns (label, first, end) positions of each
+    pass's step dispatches, and the (first, end) positions of the timed prefill's
+    dispatches."""
+    plan = [("warm-up", 3 * min(warmup, w.steps)), ("prefill", 0), ("retopk timed", steps),
             ("exact timed", steps), ("full timed", steps), ("retopk profiled", steps),
             ("exact profiled", steps), ("full profiled", steps)]
     units = {"retopk_sim": ["retopk_sim", "retopk_score", "retopk_filter", "retopk_final"],
@@ -683,14 +685,24 @@ def _passes(names, w, steps, warmup):
              "dense_chunk": ["dense_chunk", "dense_merge"]}
     out, i = [], 0
     pf = ["prefill_score", "retopk_filter", "retopk_final"]
+    prefill = None
+    n_pf = None      # triples per prefill: every handle's prefill is the same
     for label, n_units in plan:
+        p0 = i
         if names[i] == "prefill_score":
-            while names[i:i + 3] == pf:
+            if n_pf is None:   # the first handle's prefill is followed by steps
+                n_pf = 0
+                while names[i + 3 * n_pf:i + 3 * n_pf + 3] == pf:
+                    n_pf += 1
+            for _ in range(n_pf):
+                assert names[i:i + 3] == pf, f"unexpected prefill at {i}"
                 i += 3
         else:
             for _ in range(w.cache_cap):
                 assert names[i:i + 3] == units["retopk_scan"], f"unexpected prefill at {i}"
                 i += 3
+        if label == "prefill":
+            prefill = (p0, i)
         start = i
         for _ in range(n_units):
             unit = units.get(names[i])
@@ -698,7 +710,7 @@ def _passes(names, w, steps, warmup):
             i += len(unit)
         out.append((label, start, i))
     assert i == len(names), "dispatches left over"
-    return out
+    return out, prefill
 
 
 def summarize(args, trace_dir, fetch_dir, write_dir):
@@ -712,7 +724,7 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
     lib = [(r, _lib_name(r["Kernel_Name"])) for r in trace]
     lib = [(r, n) for r, n in lib if n]
     names = [n for _, n in lib]
-    passes = _passes(names, w, steps, args.warmup)
+    passes, prefill = _passes(names, w, steps, args.warmup)
     dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3  # noqa: E731
 
     lines = [f"# Kernel durations, {w.name} workload, rocprofv3 kernel trace",
@@ -720,7 +732,7 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
              "-d <out>/kt -o kt -- python3 -u <repo>/bench.py --no-cpu-baseline",
              "summary: python bench.py --summarize <out>/kt <out>/pmc_fetch <out>/pmc_write",
              "",
-             "## rocprofv3 --stats (every dispatch of the run: prefill, warm-up and the six passes)",
+             "## rocprofv3 --stats (every dispatch of the run: prefills, warm-up and the six passes)",
              f"{'kernel':60s} {'library name':14s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'share':>7s}"]
     for r in stats:
         name = _lib_name(r["Name"]) or ""
@@ -738,6 +750,13 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
             if n in acc:
                 v = acc[n]
                 lines.append(f"{label:18s} {n:14s} {len(v):8d} {sum(v) / len(v):9.2f}")
+    acc = {}
+    for r, n in lib[prefill[0]:prefill[1]]:
+        acc.setdefault(n, []).append(dur(r))
+    lines += ["", f"## prefill initialisation, {w.cache_cap} prompt-tail positions (timed handle)",
+              f"{'kernel':14s} {'launches':>8s} {'avg_us':>9s} {'sum_us':>9s}"]
+    for n, v in acc.items():
+        lines.append(f"{n:14s} {len(v):8d} {sum(v) / len(v):9.2f} {sum(v):9.1f}")
     kt_path = os.path.join(ROOT, "profiles", f"kernels_{w.name}.txt")
 
     # ---- counters: FETCH_SIZE / WRITE_SIZE, scaled by the copy calibration ----
@@ -758,7 +777,10 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
     w_factor = copy_kib / (sum(w_big) / len(w_big))
     digest = kernel_source_digest()
     written = [kt_path]
-    for kernel, pass_idx in (("retopk_score", 1), ("retopk_scan", 2), ("dense_chunk", 3)):
+    by_label = {lab: i for i, (lab, _, _) in enumerate(passes)}
+    for kernel, label in (("retopk_score", "retopk timed"), ("retopk_scan", "exact timed"),
+                          ("dense_chunk", "full timed")):
+        pass_idx = by_label[label]
         _, a, b = passes[pass_idx]
         fv = [v for v, n in fetch[a:b] if n == kernel]
         wv = [v for v, n in write[a:b] if n == kernel]
