@@ -73,6 +73,10 @@ WORKLOADS = {
     # The headline layer: 128K context, K=512.
     "128k": Workload("128k", 1, 32, 8, 128, "bf16", 131072, 256, 512, 512, 8, 256, 0.8, 64, 256,
                      0.9, 0.05),
+    # The headline layer with the paper's default selector settings (Sec. 4.1:
+    # C = W = 32, R = 4, tau = 0.85, T_r = 128).
+    "128k_paper": Workload("128k_paper", 1, 32, 8, 128, "bf16", 131072, 256, 512, 32, 4, 32,
+                           0.85, 128, 256, 0.9, 0.05),
     # Fallback-heavy: four sequences at 64K, frequent jumps, tau = 0.9.
     "stress": Workload("stress", 4, 32, 8, 128, "bf16", 65536, 256, 1024, 512, 8, 256, 0.9, 16,
                        256, 0.9, 0.3),

@@ -140,7 +140,7 @@ def test_decode_lockstep_16k_two_groups():
     assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * w.steps
 
 
-@pytest.mark.parametrize("name", ["32k", "128k", "stress"])
+@pytest.mark.parametrize("name", ["32k", "128k", "128k_paper", "stress"])
 def test_decode_full_size_sampled(name):
     """Full-size layer shapes: the cache starts from the prompt-tail queries with
     seeded supports (no prefill), and 3 steps run in lock-step; KV group 0 of the
@@ -241,6 +241,8 @@ VARIANTS = [
     ("no_refresh", dict(refresh=0), {}),   # refresh off
     ("no_window", dict(window=0), {}),     # supports only; fewer than K candidates occur
     ("always_fallback", dict(tau=2.0), {}),
+    # the paper's default selector settings (C = W = 32, R = 4, tau = 0.85, T_r = 128)
+    ("paper_defaults", dict(cache_cap=32, r=4, window=32, tau=0.85, refresh=128), {}),
 ]
 
 
