@@ -25,3 +25,44 @@ def test_cosine():
     assert abs(bench.cosine([1, 0], [1, 0]) - 1.0) < 1e-12
     assert abs(bench.cosine([1, 0], [0, 1])) < 1e-12
     assert abs(bench.cosine([1, 1], [2, 2]) - 1.0) < 1e-12
+
+
+def _dispatches(w, steps, warmup, n_pf, exact_heads_at=()):
+    """A dispatch-name sequence in the order bench.py issues it: every handle's
+    batched prefill (n_pf triples), the warm-up's three step kinds per step, the
+    timed prefill alone, then the six passes."""
+    pf = ["prefill_score", "retopk_filter", "retopk_final"]
+    sel = ["retopk_sim", "retopk_score", "retopk_filter", "retopk_final"]
+    scan = ["retopk_scan", "retopk_filter", "retopk_final"]
+    dense = ["dense_chunk", "dense_merge"]
+    names = pf * n_pf
+    for t in range(min(warmup, w.steps)):
+        names += (scan if t in exact_heads_at else sel) + scan + dense
+    names += pf * n_pf                                   # the timed prefill
+    for kind in ("retopk", "exact", "full", "retopk", "exact", "full"):
+        names += pf * n_pf
+        for t in range(steps):
+            names += {"retopk": scan if t in exact_heads_at else sel, "exact": scan,
+                      "full": dense}[kind]
+    return names
+
+
+def test_passes_split_the_dispatch_sequence():
+    from paper_2607_27692_amd.inputs import WORKLOADS
+    w = WORKLOADS["128k"]
+    steps, warmup, n_pf = 5, 2, 13
+    names = _dispatches(w, steps, warmup, n_pf, exact_heads_at=(3,))
+    passes, prefill = bench._passes(names, w, steps, warmup)
+    labels = [p[0] for p in passes]
+    assert labels == ["warm-up", "prefill", "retopk timed", "exact timed", "full timed",
+                      "retopk profiled", "exact profiled", "full profiled"]
+    assert prefill[1] - prefill[0] == 3 * n_pf
+    assert names[prefill[0]:prefill[1]] == ["prefill_score", "retopk_filter", "retopk_final"] * n_pf
+    by = {p[0]: (p[1], p[2]) for p in passes}
+    a, b = by["retopk timed"]
+    assert b - a == 4 * (steps - 1) + 3                  # one refresh-like step
+    a, b = by["exact timed"]
+    assert names[a:b] == ["retopk_scan", "retopk_filter", "retopk_final"] * steps
+    a, b = by["full timed"]
+    assert names[a:b] == ["dense_chunk", "dense_merge"] * steps
+    assert by["prefill"][0] == by["prefill"][1]          # no steps in the prefill pass
