@@ -126,6 +126,34 @@ def test_decode_lockstep_small():
     assert tally.exact >= w.steps - 2
 
 
+SHAPES = [
+    # label, workload changes: other dtypes, head sizes and group sizes than the
+    # headline layer, every head checked on every step
+    ("bf16_d64_g8", dict(n_q_heads=8, n_kv_heads=1, head_dim=64, prompt_len=4000, steps=48,
+                         k=64, cache_cap=48, r=4, window=32, refresh=16, n_centers=16)),
+    ("bf16_d128_g1_b2", dict(batch=2, n_q_heads=2, n_kv_heads=2, prompt_len=3000, steps=48,
+                             k=100, cache_cap=40, r=3, window=48, refresh=20, n_centers=12)),
+    ("f32_d128_g2", dict(dtype="f32", n_q_heads=4, n_kv_heads=2, prompt_len=2500, steps=48,
+                         k=64, cache_cap=32, r=4, window=40, refresh=12, n_centers=12)),
+]
+
+
+@pytest.mark.parametrize("label, change", SHAPES, ids=[s_[0] for s_ in SHAPES])
+def test_decode_lockstep_shapes(label, change):
+    """d = 64 with eight query heads per KV head, one query head per KV head over
+    two sequences, and fp32 at d = 128: all heads, all steps, in lock-step from
+    the oracle's prefill state."""
+    w = WORKLOADS["16k"].with_(**change)
+    print(f"decode lock-step {label}", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w)
+    heads = list(range(w.batch * w.n_q_heads))
+    tally, paths = _lockstep(w, inp, p, heads, w.steps)
+    print(tally, flush=True)
+    assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * w.steps
+    assert (paths == O.REUSE).sum() > 0
+
+
 def test_decode_lockstep_16k_two_groups():
     """32 query heads on 8 KV heads at 16K, bf16: KV groups 0 and 7 (8 query heads)
     checked on all 128 steps."""
