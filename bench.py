@@ -143,8 +143,10 @@ def main():
     h.close()
     log(f"[bench] prefill initialisation: {pf_ms:.2f} ms")
 
-    def timed(run, profile):
+    def timed(run, profile, flush_between=None):
         """One pass over the timed steps on a fresh handle (prefill untimed)."""
+        if flush_between is None:
+            flush_between = not args.warm
         handle = fresh_handle()
         st0 = handle.stats()
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -153,7 +155,7 @@ def main():
         torch.cuda.synchronize()
         wall0 = time.perf_counter()
         for t in range(K_steps):
-            if not args.warm:
+            if flush_between:
                 sink.add_(flush.sum())
             ev[t][0].record(stream)
             run(handle, t)
@@ -184,6 +186,27 @@ def main():
     _, _, e_prof, _ = timed(exact_run, True)
     _, _, f_prof, _ = timed(full_run, True)
     assert st_p == st, "profiled pass diverged from the timed pass"
+    # The same two passes back to back, without the flush (warm caches).
+    rw_ms = timed(retopk_run, False, flush_between=False)[0]
+    ew_ms = timed(exact_run, False, flush_between=False)[0]
+    log(f"[bench] warm: ReTopK {rw_ms.mean() * 1e3:.1f} us/step, Exact {ew_ms.mean() * 1e3:.1f}")
+    # The kind of every timed step (the trajectory is deterministic): an untimed
+    # pass that reads the counters after each step.
+    hh = fresh_handle()
+    kinds, prev = [], hh.stats()
+    for t in range(K_steps):
+        retopk_run(hh, t)
+        cur = hh.stats()
+        dlt = {k_: cur[k_] - prev[k_] for k_ in cur}
+        prev = cur
+        kinds.append("refresh" if dlt["refresh"] else ("no_scan" if dlt["kv_group_scans"] == 0 else
+                     ("one_scan" if dlt["kv_group_scans"] == 1 else "scans_2plus")))
+    hh.close()
+    kinds = np.array(kinds)
+    step_types = {kd: {"steps": int((kinds == kd).sum()),
+                       "us_mean": round(float(r_ms[kinds == kd].mean()) * 1e3, 2),
+                       "us_median": round(float(np.median(r_ms[kinds == kd])) * 1e3, 2)}
+                  for kd in ("no_scan", "one_scan", "scans_2plus", "refresh") if (kinds == kd).any()}
 
     # ---- algorithmic bytes ------------------------------------------------------
     e = 2 if w.dtype == "bf16" else 4
@@ -327,6 +350,10 @@ def main():
         "exact_roofline": exact_roof,
         "full_attention_roofline": full_roof,
         "prefill_init": prefill,
+        "step_types": step_types,
+        "warm_caches": {"retopk_us_per_step": round(float(rw_ms.mean()) * 1e3, 2),
+                        "exact_us_per_step": round(float(ew_ms.mean()) * 1e3, 2),
+                        "speedup_vs_exact": round(float(ew_ms.mean() / rw_ms.mean()), 3)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
@@ -674,12 +701,14 @@ def _passes(names, w, steps, warmup):
     issues sim, score, filter, final, any other step or an Exact Top-K step
     scan, filter, final, and a full-attention step dense_chunk, dense_merge.
     The warm-up runs one step of each kind per warm-up step, then one handle
-    runs the timed prefill alone.  Returns (label, first, end) positions of each
+    runs the timed prefill alone; after the six passes come the two warm-cache
+    passes and the untimed pass that labels the step kinds.  Returns (label, first, end) positions of each
     pass's step dispatches, and the (first, end) positions of the timed prefill's
     dispatches."""
     plan = [("warm-up", 3 * min(warmup, w.steps)), ("prefill", 0), ("retopk timed", steps),
             ("exact timed", steps), ("full timed", steps), ("retopk profiled", steps),
-            ("exact profiled", steps), ("full profiled", steps)]
+            ("exact profiled", steps), ("full profiled", steps), ("retopk warm", steps),
+            ("exact warm", steps), ("step kinds", steps)]
     units = {"retopk_sim": ["retopk_sim", "retopk_score", "retopk_filter", "retopk_final"],
              "retopk_scan": ["retopk_scan", "retopk_filter", "retopk_final"],
              "dense_chunk": ["dense_chunk", "dense_merge"]}
@@ -732,7 +761,7 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
              "-d <out>/kt -o kt -- python3 -u <repo>/bench.py --no-cpu-baseline",
              "summary: python bench.py --summarize <out>/kt <out>/pmc_fetch <out>/pmc_write",
              "",
-             "## rocprofv3 --stats (every dispatch of the run: prefills, warm-up and the six passes)",
+             "## rocprofv3 --stats (every dispatch of the run: prefills, warm-up and all passes)",
              f"{'kernel':60s} {'library name':14s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'share':>7s}"]
     for r in stats:
         name = _lib_name(r["Name"]) or ""

@@ -30,7 +30,8 @@ def test_cosine():
 def _dispatches(w, steps, warmup, n_pf, exact_heads_at=()):
     """A dispatch-name sequence in the order bench.py issues it: every handle's
     batched prefill (n_pf triples), the warm-up's three step kinds per step, the
-    timed prefill alone, then the six passes."""
+    timed prefill alone, the six passes, the two warm passes and the labelling
+    pass."""
     pf = ["prefill_score", "retopk_filter", "retopk_final"]
     sel = ["retopk_sim", "retopk_score", "retopk_filter", "retopk_final"]
     scan = ["retopk_scan", "retopk_filter", "retopk_final"]
@@ -39,7 +40,8 @@ def _dispatches(w, steps, warmup, n_pf, exact_heads_at=()):
     for t in range(min(warmup, w.steps)):
         names += (scan if t in exact_heads_at else sel) + scan + dense
     names += pf * n_pf                                   # the timed prefill
-    for kind in ("retopk", "exact", "full", "retopk", "exact", "full"):
+    for kind in ("retopk", "exact", "full", "retopk", "exact", "full", "retopk", "exact",
+                 "retopk"):
         names += pf * n_pf
         for t in range(steps):
             names += {"retopk": scan if t in exact_heads_at else sel, "exact": scan,
@@ -55,7 +57,8 @@ def test_passes_split_the_dispatch_sequence():
     passes, prefill = bench._passes(names, w, steps, warmup)
     labels = [p[0] for p in passes]
     assert labels == ["warm-up", "prefill", "retopk timed", "exact timed", "full timed",
-                      "retopk profiled", "exact profiled", "full profiled"]
+                      "retopk profiled", "exact profiled", "full profiled", "retopk warm",
+                      "exact warm", "step kinds"]
     assert prefill[1] - prefill[0] == 3 * n_pf
     assert names[prefill[0]:prefill[1]] == ["prefill_score", "retopk_filter", "retopk_final"] * n_pf
     by = {p[0]: (p[1], p[2]) for p in passes}
