@@ -1080,7 +1080,9 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     static_assert(kMaxRegions % NT == 0 && kCandRanges <= NT, "region ownership");
     __shared__ FinalSmem<D, NT> sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int vh = blockIdx.x / kFinalSlices, slice = blockIdx.x % kFinalSlices;
+    // the multi-position (prefill) build writes no output: one block per head
+    constexpr int NS = kMulti ? 1 : kFinalSlices;
+    const int vh = blockIdx.x / NS, slice = blockIdx.x % NS;
     const bool writes_out = a.out != nullptr && a.mode != MODE_PREFILL;
     if (slice != 0 && !writes_out) return;
     // Virtual head vh = u * B * Hq + bh: query position u of head bh (u = 0 unless
@@ -1752,7 +1754,7 @@ template <typename T, int D>
 static void final_desc(const StepArgs &a, KernelDesc *k)
 {
     *k = KernelDesc{a.U > 1 ? (const void *)&k_final<T, D, true> : (const void *)&k_final<T, D, false>,
-                    dim3((unsigned)(a.B * a.Hq * a.U * kFinalSlices)),
+                    dim3((unsigned)(a.B * a.Hq * a.U * (a.U > 1 ? 1 : kFinalSlices))),
                     dim3(kFinalThreads), 0u, 2};
 }
 
