@@ -65,6 +65,11 @@ def parse():
                          "other per token, as a model does, and report ms per token over the L "
                          "layers for ReTopK, Exact Top-K and full attention (no cache flush: "
                          "rotating the layers' key and value rows defeats the caches)")
+    ap.add_argument("--contexts", default="", metavar="N1,N2,...",
+                    help="instead of the one-layer protocol, time the headline layer at each "
+                         "prompt length given (ReTopK, Exact Top-K and full attention, cold "
+                         "caches, --steps decode steps each, at most 64) and print one JSON "
+                         "line with the per-length table (latency against context length)")
     return ap.parse_args()
 
 
@@ -86,6 +91,9 @@ def main():
         return
     if args.layers:
         layers(args)
+        return
+    if args.contexts:
+        contexts(args)
         return
     import torch
 
@@ -535,6 +543,91 @@ def fidelity(args):
     print(json.dumps({"fidelity": {"workload": w.name, "steps": steps, "data": "synthetic",
                                    "all": summary(np.ones(len(a), bool)),
                                    "reuse_path": summary(reuse)}}), flush=True)
+
+
+# ---- latency against context length -------------------------------------------
+def contexts(args):
+    """The headline layer (32 query / 8 KV heads, d = 128, bf16, K = 512, C = 512,
+    R = 8, W = 256, tau = 0.8, T_r = 64; one key cluster per K keys) at each prompt
+    length: mean us per step of
+    ReTopK, Exact Top-K and full attention under the cold-cache protocol, the
+    fallback rate and the KV-group scans per step.  The reuse path's work does not
+    depend on the context length; the exact path's grows with it (Sec. 4.3)."""
+    import torch
+
+    from paper_2607_27692_amd import retopk as R
+    from paper_2607_27692_amd.inputs import WORKLOADS, make_inputs
+
+    base = WORKLOADS["128k"]
+    steps = max(1, min(args.steps, 64))
+    torch.cuda.set_device(0)
+    flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    sink = torch.zeros((), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    dev = lambda raw: torch.from_numpy(raw.view(np.int16)).to("cuda")  # noqa: E731
+    rows = []
+    for n_ctx in [int(x) for x in args.contexts.split(",") if x]:
+        # as many key clusters as keys / K, so that a cluster is about one support
+        w = base.with_(name=f"{n_ctx // 1024}k", prompt_len=n_ctx, steps=steps,
+                       n_centers=max(1, n_ctx // base.k))
+        t0 = time.time()
+        inp = make_inputs(w)
+        q_tail, q_dec, k, v = (dev(inp.q_tail_raw), dev(inp.q_dec_raw), dev(inp.k_raw),
+                               dev(inp.v_raw))
+        del inp
+        cfg = dict(batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+                   head_dim=w.head_dim, max_len=w.max_len, k=w.k, cache_cap=w.cache_cap,
+                   r=w.r, window=w.window, tau=w.tau, refresh=w.refresh, dtype=w.dtype)
+        out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32,
+                          device="cuda")
+        sel = torch.empty((w.batch, w.n_q_heads, w.k), dtype=torch.int32, device="cuda")
+
+        def one_pass(kind, prefill):
+            h = R.Handle(**cfg)
+            if prefill:
+                h.prefill_init(q_tail, w.cache_cap, k, v, w.prompt_len)
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(steps)]
+            st0 = h.stats()
+            torch.cuda.synchronize()
+            for t in range(steps):
+                sink.add_(flush.sum())
+                ev[t][0].record(stream)
+                if kind == "retopk":
+                    h.decode_step(q_dec[t], k, v, w.step_len(t), out, sel)
+                elif kind == "exact":
+                    h.exact(q_dec[t], k, v, w.step_len(t), out, sel)
+                else:
+                    h.full(q_dec[t], k, v, w.step_len(t), out)
+                ev[t][1].record(stream)
+            torch.cuda.synchronize()
+            st1 = h.stats()
+            h.close()
+            ms = np.array([a.elapsed_time(b) for a, b in ev])
+            return ms, {k_: st1[k_] - st0[k_] for k_ in st1}
+
+        one_pass("retopk", True)     # warm-up: kernels loaded, allocator primed
+        r_ms, st = one_pass("retopk", True)
+        e_ms, _ = one_pass("exact", False)
+        f_ms, _ = one_pass("full", False)
+        row = {"context": n_ctx, "retopk_us": round(float(r_ms.mean()) * 1e3, 2),
+               "retopk_us_median": round(float(np.median(r_ms)) * 1e3, 2),
+               "exact_us": round(float(e_ms.mean()) * 1e3, 2),
+               "full_attention_us": round(float(f_ms.mean()) * 1e3, 2),
+               "speedup_vs_exact": round(float(e_ms.mean() / r_ms.mean()), 3),
+               "fallback_rate": round(st["fallback"] / st["head_steps"], 4),
+               "kv_group_scans_per_step": round(st["kv_group_scans"] / steps, 3)}
+        rows.append(row)
+        log(f"[contexts] {n_ctx}: {row} ({time.time() - t0:.1f}s)")
+        del q_tail, q_dec, k, v
+        torch.cuda.empty_cache()
+    print(json.dumps({"contexts": rows, "steps": steps, "data": "synthetic", "dtype": "bf16",
+                      "config": {"batch": base.batch, "q_heads": base.n_q_heads,
+                                 "kv_heads": base.n_kv_heads, "head_dim": base.head_dim,
+                                 "k": base.k, "cache_cap": base.cache_cap, "r": base.r,
+                                 "window": base.window, "tau": base.tau,
+                                 "refresh": base.refresh},
+                      "cache_state": "cold (1 GiB read between steps)"}), flush=True)
 
 
 # ---- several layers per token ---------------------------------------------------
