@@ -134,7 +134,13 @@ Geometry make_geometry(const retopk_handle_s *h, int64_t len, int mode)
     // fewer in MODE_SELECT, where the range blocks share the chip.
     const int64_t rows = (int64_t)c.batch * c.n_kv_heads * len;
     const int64_t want = ceil_div(rows, 2 * kScanRowsPerIter);
-    const int cap = mode == MODE_SELECT ? kScanBlocksSelect : kScanBlocksExact;
+    // In MODE_SELECT the scan shares the launch with the range blocks and covers
+    // only the groups with a fallback head: a fixed number of blocks per KV group,
+    // so that a step where most groups fall back still spreads over the chip.
+    int64_t sel_cap = (int64_t)kScanBlocksPerGroup * c.batch * c.n_kv_heads;
+    sel_cap = sel_cap < kScanBlocksSelect ? kScanBlocksSelect
+                                          : (sel_cap > kScanBlocksExact ? kScanBlocksExact : sel_cap);
+    const int cap = mode == MODE_SELECT ? (int)sel_cap : kScanBlocksExact;
     g.scan_blocks = (int)(want < cap ? want : cap);
     g.cand_blocks = mode == MODE_SELECT ? (int)(heads_of(c) * kCandRanges) : 0;
     g.filter_blocks_per_head = (int)ceil_div(len, kFilterRows);

@@ -28,7 +28,8 @@ constexpr int kMaxK = 2048;
 constexpr int kMaxR = 32;
 constexpr int kMaxCache = 4096;
 constexpr int kMaxHeads = 2048;       // B * Hq
-constexpr int kScanBlocksSelect = 256;  // k_score scan blocks in MODE_SELECT
+constexpr int kScanBlocksSelect = 256;  // k_score scan blocks in MODE_SELECT: at least this,
+constexpr int kScanBlocksPerGroup = 32; // or this many per KV group (capped at kScanBlocksExact)
 constexpr int kScanBlocksExact = 2048;  // k_score scan blocks when every head is exact
 constexpr int64_t kMaxLen = (int64_t)kMaxRegions * kFilterRows;
 
