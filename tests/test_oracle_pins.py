@@ -551,3 +551,59 @@ def test_recent_r_equals_similarity_when_all_entries_are_retrieved(oracle_lib, t
         assert np.array_equal(ia.path, ib.path)
         assert np.array_equal(sa, sb)
         assert np.array_equal(oa, ob)
+
+
+def test_top_r_retrieval_bruteforce(oracle_lib, tiny):
+    """Eq. 6-7 by brute force on every step that computes similarities: rho_c is the
+    cosine of q with each valid cached q_bar (computed here in float64 from the
+    stored fp32 rows), rho_max their maximum, and the retrieved entries the R most
+    similar, ties to the newer insertion, most similar first; the candidates are
+    the union of their supports and the window (Eq. 8-9)."""
+    w = tiny.w
+    p = _workload_params(w)
+    seen = {"reuse": 0, "fallback": 0}
+
+    def check(t, before, out, sel, info):
+        path = int(info.path[0])
+        if path not in (O.REUSE, O.FALLBACK):
+            return
+        nv = min(before["n_inserted"], w.cache_cap)
+        q = tiny.q_dec[t][0, 0].astype(np.float64)
+        qb = (q / np.sqrt((q * q).sum())).astype(np.float32).astype(np.float64)
+        rho = before["qbar"][0, :nv].astype(np.float64) @ qb
+        age = [(before["n_inserted"] - 1 - s) % w.cache_cap for s in range(nv)]
+        order = sorted(range(nv), key=lambda s: (-rho[s], age[s]))
+        assert abs(info.rho_max[0] - rho.max()) <= 1e-12 * max(1.0, abs(rho.max()))
+        assert (path == O.FALLBACK) == (rho.max() < w.tau)
+        if path == O.FALLBACK:
+            seen["fallback"] += 1
+            return
+        seen["reuse"] += 1
+        n_ret = min(w.r, nv)
+        assert info.retrieved[0, :n_ret].tolist() == order[:n_ret]
+        L = w.step_len(t)
+        union = set(range(max(0, L - w.window), L))
+        for s in order[:n_ret]:
+            union.update(before["supp"][0, s, :before["cnt"][0, s]].tolist())
+        n = int(info.n_cand[0])
+        assert info.cand[0, :n].tolist() == sorted(union)
+
+    _run(w, tiny, p, check=check)
+    assert seen["reuse"] > 10 and seen["fallback"] > 0
+
+
+def test_softmax_v_is_a_convex_combination(oracle_lib, tiny):
+    """Eq. 12: the output is a convex combination of the selected value rows, so
+    every coordinate lies between the smallest and the largest selected value of
+    that coordinate (a wrong normalisation or sign breaks this)."""
+    w = tiny.w
+    p = _workload_params(w)
+    for t in (0, 7, 31):
+        L = w.step_len(t)
+        out, sel, _ = O.exact(p, tiny.q_dec[t], tiny.k, tiny.v, L)
+        idx = sel[0, 0][sel[0, 0] >= 0]
+        vs = tiny.v[0, 0, idx].astype(np.float64)
+        o = out[0, 0].astype(np.float64)
+        slack = 1e-6 * np.abs(vs).max()
+        assert (o >= vs.min(axis=0) - slack).all() and (o <= vs.max(axis=0) + slack).all()
+        assert len(idx) == min(w.k, L)
