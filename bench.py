@@ -309,6 +309,24 @@ def main():
                "prefill_score_tflops": round(pf_flops / (pf_score[1] * 1e-3) / 1e12, 1)
                if pf_score[0] else None}
 
+    # ---- the practical HBM read ceiling: a plain streaming read of 1 GiB -------
+    sink32 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    nbytes = flush.numel() * flush.element_size()
+    for _ in range(2):
+        R.retopk_stream_read(flush, nbytes, sink32)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(10):
+        R.retopk_stream_read(flush, nbytes, sink32)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    stream_gbs = 10 * nbytes / (ev0.elapsed_time(ev1) * 1e-3) / 1e9
+    log(f"[bench] streaming read: {stream_gbs:.0f} GB/s")
+    for rf in (roof, exact_roof, full_roof):
+        if rf:
+            rf["stream_read_gbs"] = round(stream_gbs, 1)
+            rf["frac_of_stream_read"] = round(rf["achieved"] / stream_gbs, 4)
+
     # ---- CPU baseline: the oracle on a bounded sample ------------------------
     cpu = None
     if not args.no_cpu_baseline:

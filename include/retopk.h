@@ -147,6 +147,14 @@ retopk_status retopk_decode_step(retopk_handle h, const void *q, const void *k, 
 retopk_status full_attention(retopk_handle h, const void *q, const void *k, const void *v,
                              int64_t len, float *out, void *stream);
 
+/* Measurement aid (no part of the method): reads `bytes` of device memory at `src`
+ * once with a plain streaming kernel, the practical HBM read ceiling that the
+ * benchmark reports beside the published peak.  src must be 16-byte aligned and
+ * bytes a multiple of 16; *sink (device, 4 bytes) is written only if the data
+ * XOR to a value no real buffer of this size is expected to give, so that the
+ * reads are kept.  Asynchronous on `stream`. */
+retopk_status retopk_stream_read(const void *src, int64_t bytes, uint32_t *sink, void *stream);
+
 /* Exact Top-K attention (Eq. 1 with Eq. 4, then Eq. 12) for every head over rows
  * [0, len): the full-history baseline.  Uses the handle's workspaces only; the
  * caches and counters are untouched. */

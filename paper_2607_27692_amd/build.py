@@ -9,7 +9,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libretopk.so")
-SOURCES = [os.path.join(CSRC, "retopk_kernels.hip"), os.path.join(CSRC, "retopk_api.hip")]
+SOURCES = [os.path.join(CSRC, "retopk_kernels.hip"), os.path.join(CSRC, "retopk_api.hip"),
+           os.path.join(CSRC, "retopk_stream.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

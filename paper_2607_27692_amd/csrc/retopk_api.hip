@@ -504,6 +504,13 @@ retopk_status retopk_prefill_init(retopk_handle h, const void *q_tail, int32_t n
     return RETOPK_OK;
 }
 
+retopk_status retopk_stream_read(const void *src, int64_t bytes, uint32_t *sink, void *stream)
+{
+    if (!src || !sink || bytes <= 0 || bytes % 16 != 0 || !aligned16(src)) return RETOPK_ERR_ARG;
+    launch_stream_read(src, bytes, sink, (hipStream_t)stream);
+    return hipGetLastError() == hipSuccess ? RETOPK_OK : RETOPK_ERR_HIP;
+}
+
 retopk_status full_attention(retopk_handle h, const void *q, const void *k, const void *v,
                              int64_t len, float *out, void *stream)
 {

@@ -151,5 +151,7 @@ constexpr int kMergeThreads = 1024;  // dense merge block: one per query head
 // dtype: 0 = f32, 1 = bf16.
 void describe_kernel(int which, int dtype, const StepArgs &a, const Geometry &geo, KernelDesc *k);
 bool shape_supported(int dtype, int d, int g);
+// Streaming read of `bytes` at src (a measurement aid; retopk_stream.hip).
+void launch_stream_read(const void *src, int64_t bytes, uint32_t *sink, hipStream_t s);
 
 }  // namespace retopk

@@ -20,7 +20,8 @@ STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape", -3: "device 
 
 # Every symbol include/retopk.h declares.
 EXPORTS = ("retopk_create", "retopk_destroy", "retopk_prefill_init", "retopk_decode_step",
-           "exact_topk_attention", "full_attention", "retopk_stats", "retopk_get_state",
+           "exact_topk_attention", "full_attention", "retopk_stream_read", "retopk_stats",
+           "retopk_get_state",
            "retopk_set_state",
            "retopk_profile", "retopk_profile_read", "retopk_kernel_name",
            "retopk_status_string")
@@ -72,6 +73,7 @@ def load(path: str | None = None):
         "retopk_decode_step": ([P, P, P, P, I64, P, P, C.POINTER(retopk_debug), P], C.c_int),
         "exact_topk_attention": ([P, P, P, P, I64, P, P, P], C.c_int),
         "full_attention": ([P, P, P, P, I64, P, P], C.c_int),
+        "retopk_stream_read": ([P, I64, P, P], C.c_int),
         "retopk_stats": ([P, C.POINTER(retopk_stats_t)], C.c_int),
         "retopk_get_state": ([P, P, P, P, C.POINTER(I64), C.POINTER(I64)], C.c_int),
         "retopk_set_state": ([P, P, P, P, I64, I64], C.c_int),
@@ -157,6 +159,12 @@ def exact_topk_attention(h, q, k, v, length, out, sel=None, stream=None) -> None
 def full_attention(h, q, k, v, length, out, stream=None) -> None:
     _check("full_attention", load().full_attention(
         h, _addr(q), _addr(k), _addr(v), length, _addr(out), _stream(stream)))
+
+
+def retopk_stream_read(src, nbytes: int, sink, stream=None) -> None:
+    """Read nbytes at src once (the streaming-read ceiling; a measurement aid)."""
+    _check("retopk_stream_read", load().retopk_stream_read(_addr(src), nbytes, _addr(sink),
+                                                            _stream(stream)))
 
 
 def retopk_stats(h) -> dict:

@@ -72,6 +72,12 @@ def test_null_arguments(lib):
     assert lib.retopk_decode_step(None, 16, 16, 16, 1, 16, None, None, None) == -1
     assert lib.exact_topk_attention(None, 16, 16, 16, 1, 16, None, None) == -1
     assert lib.full_attention(None, 16, 16, 16, 1, 16, None) == -1
+    # argument checks of the streaming read happen before any HIP call
+    assert lib.retopk_stream_read(None, 16, 16, None) == -1
+    assert lib.retopk_stream_read(16, 16, None, None) == -1
+    assert lib.retopk_stream_read(16, 24, 16, None) == -1      # not a multiple of 16
+    assert lib.retopk_stream_read(8, 16, 16, None) == -1       # not 16-byte aligned
+    assert lib.retopk_stream_read(16, 0, 16, None) == -1
     assert lib.retopk_prefill_init(None, 16, 1, 16, 16, 1, None) == -1
     st = R.retopk_stats_t()
     assert lib.retopk_stats(None, C.byref(st)) == -1

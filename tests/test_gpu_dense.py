@@ -10,6 +10,7 @@ import pytest
 
 from gpu_harness import OUT_TOL, handle_of, rel_err, to_dev, torch_cuda
 from oracle import oracle as O
+from paper_2607_27692_amd import retopk as R
 from paper_2607_27692_amd.inputs import bf16_bits_to_f32, to_bf16_bits
 
 pytestmark = pytest.mark.gpu
@@ -56,3 +57,14 @@ def test_full_attention_parity(dtype, d, B, Hq, Hkv, L):
             worst = max(worst, e)
             assert e <= OUT_TOL[dtype], f"b={b} h={hq}: relative error {e:.3g}"
     print(f"max relative error {worst:.3g}", flush=True)
+
+
+def test_stream_read_runs():
+    """The streaming-read measurement aid reads a buffer and leaves the sink alone
+    (the fold of a buffer of equal words is 0, not the sentinel)."""
+    torch = torch_cuda()
+    x = torch.ones(1 << 20, dtype=torch.float32, device="cuda")
+    sink = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    R.retopk_stream_read(x, x.numel() * 4, sink)
+    torch.cuda.synchronize()
+    assert int(sink.item()) == 7
