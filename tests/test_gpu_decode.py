@@ -135,14 +135,21 @@ SHAPES = [
                              k=100, cache_cap=40, r=3, window=48, refresh=20, n_centers=12)),
     ("f32_d128_g2", dict(dtype="f32", n_q_heads=4, n_kv_heads=2, prompt_len=2500, steps=48,
                          k=64, cache_cap=32, r=4, window=40, refresh=12, n_centers=12)),
+    # the largest cache and R the library takes (64 similarity lists of 32)
+    ("f32_c4096_r32", dict(dtype="f32", n_q_heads=1, n_kv_heads=1, head_dim=64, prompt_len=6000,
+                           steps=24, k=64, cache_cap=4096, r=32, window=64, refresh=8,
+                           n_centers=12)),
+    # the largest K
+    ("bf16_k2048", dict(n_q_heads=2, n_kv_heads=1, prompt_len=9000, steps=16, k=2048,
+                        cache_cap=16, r=2, window=128, refresh=8, n_centers=8)),
 ]
 
 
 @pytest.mark.parametrize("label, change", SHAPES, ids=[s_[0] for s_ in SHAPES])
 def test_decode_lockstep_shapes(label, change):
     """d = 64 with eight query heads per KV head, one query head per KV head over
-    two sequences, and fp32 at d = 128: all heads, all steps, in lock-step from
-    the oracle's prefill state."""
+    two sequences, fp32 at d = 128, the largest cache with the largest R, and the
+    largest K: all heads, all steps, in lock-step from the oracle's prefill state."""
     w = WORKLOADS["16k"].with_(**change)
     print(f"decode lock-step {label}", flush=True)
     inp = make_inputs(w)
