@@ -70,6 +70,11 @@ def parse():
                          "prompt length given (ReTopK, Exact Top-K and full attention, cold "
                          "caches, --steps decode steps each, at most 64) and print one JSON "
                          "line with the per-length table (latency against context length)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="instead of the one-layer protocol, run the component-ablation "
+                         "settings (Table 3) and the paper's default settings on the 128K "
+                         "layer: us per step, exact-path share, candidates, speedup against "
+                         "Exact Top-K and support recall, one JSON line")
     return ap.parse_args()
 
 
@@ -94,6 +99,9 @@ def main():
         return
     if args.contexts:
         contexts(args)
+        return
+    if args.ablation:
+        ablation(args)
         return
     import torch
 
@@ -561,6 +569,107 @@ def fidelity(args):
     print(json.dumps({"fidelity": {"workload": w.name, "steps": steps, "data": "synthetic",
                                    "all": summary(np.ones(len(a), bool)),
                                    "reuse_path": summary(reuse)}}), flush=True)
+
+
+# ---- component ablation (Table 3) ----------------------------------------------
+ABLATION = [  # label, config changes (the same inputs for every setting)
+    ("retopk", {}),
+    ("recent_r", {"retrieval": 1}),
+    ("r1", {"r": 1}),
+    ("c1", {"cache_cap": 1}),
+    ("tau_minus1", {"tau": -1.0}),
+    ("no_refresh", {"refresh": 0}),
+    ("no_window", {"window": 0}),
+    ("paper_defaults", {"cache_cap": 32, "r": 4, "window": 32, "tau": 0.85, "refresh": 128}),
+]
+
+
+def ablation(args):
+    """The settings of the paper's component ablation (Table 3) on the 128K layer,
+    each on the same keys, values and queries (the prefill uses the last C prompt
+    queries): mean us per step (cold caches), the share of head-steps on the exact
+    path, mean candidates per reuse head, the speedup against Exact Top-K, and the
+    support recall against Exact Top-K over the first steps."""
+    import torch
+
+    from paper_2607_27692_amd import retopk as R
+    from paper_2607_27692_amd.inputs import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    steps = min(args.steps, w.steps)
+    rsteps = min(16, steps)
+    torch.cuda.set_device(0)
+    inp = make_inputs(w)
+
+    def dev(raw):
+        if raw.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(raw).view(np.int16)).to("cuda")
+        return torch.from_numpy(np.ascontiguousarray(raw)).to("cuda")
+
+    q_dec, k, v = dev(inp.q_dec_raw), dev(inp.k_raw), dev(inp.v_raw)
+    flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    sink = torch.zeros((), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    base = dict(batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+                head_dim=w.head_dim, max_len=w.max_len, k=w.k, cache_cap=w.cache_cap, r=w.r,
+                window=w.window, tau=w.tau, refresh=w.refresh, dtype=w.dtype)
+    out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    sel = torch.empty((w.batch, w.n_q_heads, w.k), dtype=torch.int32, device="cuda")
+
+    def timed(run):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+        torch.cuda.synchronize()
+        for t in range(steps):
+            sink.add_(flush.sum())
+            ev[t][0].record(stream)
+            run(t)
+            ev[t][1].record(stream)
+        torch.cuda.synchronize()
+        return np.array([a.elapsed_time(b) for a, b in ev]) * 1e3
+
+    # Exact Top-K: time, and its supports for the recall
+    he = R.Handle(**base)
+    exact_sel = []
+    for t in range(rsteps):
+        he.exact(q_dec[t], k, v, w.step_len(t), out, sel)
+        exact_sel.append(sel.cpu().numpy().copy())
+    e_us = timed(lambda t: he.exact(q_dec[t], k, v, w.step_len(t), out, sel)).mean()
+    he.close()
+    rows = []
+    for label, change in ABLATION:
+        cfg = dict(base, **change)
+        C = cfg["cache_cap"]
+        q_tail = dev(inp.q_tail_raw[:, :, w.cache_cap - C:])
+        # support recall over the first steps, then the timed pass, each from the prefill
+        h = R.Handle(**cfg)
+        h.prefill_init(q_tail, C, k, v, w.prompt_len)
+        rec = []
+        for t in range(rsteps):
+            h.decode_step(q_dec[t], k, v, w.step_len(t), out, sel)
+            s_ = sel.cpu().numpy()
+            rec += [support_recall(s_[b, hq], exact_sel[t][b, hq])
+                    for b in range(w.batch) for hq in range(w.n_q_heads)]
+        h.close()
+        h = R.Handle(**cfg)
+        h.prefill_init(q_tail, C, k, v, w.prompt_len)
+        st0 = h.stats()
+        r_us = timed(lambda t: h.decode_step(q_dec[t], k, v, w.step_len(t), out, sel))
+        st = {k_: v_ - st0[k_] for k_, v_ in h.stats().items()}
+        h.close()
+        hs = st["head_steps"]
+        row = {"setting": label, **change, "us_per_step": round(float(r_us.mean()), 2),
+               "speedup_vs_exact": round(float(e_us / r_us.mean()), 3),
+               "exact_path_share": round((st["fallback"] + st["refresh"] + st["cold"]) / hs, 4),
+               "fallback_rate": round(st["fallback"] / hs, 4),
+               "mean_candidates": round(st["cand_sum"] / st["reuse"], 1) if st["reuse"] else None,
+               "support_recall": round(float(np.mean(rec)), 4)}
+        rows.append(row)
+        log(f"[ablation] {row}")
+    print(json.dumps({"ablation": rows, "workload": w.name, "steps": steps,
+                      "recall_steps": rsteps, "exact_us_per_step": round(float(e_us), 2),
+                      "data": "synthetic", "cache_state": "cold (1 GiB read between steps)"}),
+          flush=True)
 
 
 # ---- latency against context length -------------------------------------------
