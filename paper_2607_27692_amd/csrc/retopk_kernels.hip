@@ -934,6 +934,35 @@ struct Regions {
     }
 };
 
+// Descending scan of sm.hist (nb <= kHistBins bins): the bin where the count
+// from the top reaches k (found_digit), the count above it and its own count.
+// Thread t covers bins nb-1-BPT*t .. nb-BPT-BPT*t.
+template <int D, int NT>
+__device__ void find_bin(FinalSmem<D, NT> &sm, uint32_t nb, uint32_t k)
+{
+    constexpr int BPT = (kHistBins + NT - 1) / NT;
+    const int tid = threadIdx.x;
+    uint32_t c[BPT], mine = 0;
+#pragma unroll
+    for (int j = 0; j < BPT; ++j) {
+        const int dgt = (int)nb - 1 - BPT * tid - j;
+        c[j] = dgt >= 0 ? sm.hist[dgt] : 0u;
+        mine += c[j];
+    }
+    uint32_t all;
+    uint32_t above = block_excl_scan<NT>(mine, sm.redu, &all);
+#pragma unroll
+    for (int j = 0; j < BPT; ++j) {
+        if (above < k && above + c[j] >= k) {
+            sm.found_digit = nb - 1u - (uint32_t)(BPT * tid + j);
+            sm.found_above = above;
+            sm.found_cnt = c[j];
+        }
+        above += c[j];
+    }
+    __syncthreads();
+}
+
 // Radix select over distinct 64-bit ranks with 11-bit digits, most significant
 // first, starting at the highest bit in which the ranks differ (rmax ^ rmin).
 // On return the top min(K, n) entries are exactly those with
@@ -964,25 +993,7 @@ __device__ void radix_threshold(const Regions &rg, int K, FinalSmem<D, NT> &sm, 
             if ((e & mask) == prefix) atomicAdd(&sm.hist[(uint32_t)(e >> sh) & (nb - 1u)], 1u);
         }
         __syncthreads();
-        // thread t covers digits nb-1-4t .. nb-4-4t (descending)
-        uint32_t c[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int dgt = (int)nb - 1 - 4 * tid - j;
-            c[j] = dgt >= 0 ? sm.hist[dgt] : 0u;
-        }
-        uint32_t all;
-        uint32_t above = block_excl_scan<NT>(c[0] + c[1] + c[2] + c[3], sm.redu, &all);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (above < k_rem && above + c[j] >= k_rem) {
-                sm.found_digit = nb - 1u - 4u * tid - j;
-                sm.found_above = above;
-                sm.found_cnt = c[j];
-            }
-            above += c[j];
-        }
-        __syncthreads();
+        find_bin<D, NT>(sm, nb, k_rem);
         k_rem -= sm.found_above;
         prefix |= (uint64_t)sm.found_digit << sh;
         mask |= (uint64_t)(nb - 1u) << sh;
@@ -990,32 +1001,6 @@ __device__ void radix_threshold(const Regions &rg, int K, FinalSmem<D, NT> &sm, 
         __syncthreads();
         if (done) break;
     }
-}
-
-// Descending scan of sm.hist (nb <= 4 * NT bins): the bin where the count from
-// the top reaches k (found_digit), the count above it and its own count.
-template <int D, int NT>
-__device__ void find_bin(FinalSmem<D, NT> &sm, uint32_t nb, uint32_t k)
-{
-    const int tid = threadIdx.x;
-    uint32_t c[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int dgt = (int)nb - 1 - 4 * tid - j;
-        c[j] = dgt >= 0 ? sm.hist[dgt] : 0u;
-    }
-    uint32_t all;
-    uint32_t above = block_excl_scan<NT>(c[0] + c[1] + c[2] + c[3], sm.redu, &all);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        if (above < k && above + c[j] >= k) {
-            sm.found_digit = nb - 1u - 4u * tid - j;
-            sm.found_above = above;
-            sm.found_cnt = c[j];
-        }
-        above += c[j];
-    }
-    __syncthreads();
 }
 
 // Threshold rank of the Top-K over the n staged entries (n > K): the K-th largest
