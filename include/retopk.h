@@ -67,7 +67,7 @@ typedef enum {
 typedef struct {
     int32_t batch;       /* B >= 1                                               */
     int32_t n_q_heads;   /* Hq >= 1                                              */
-    int32_t n_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0, Hq / Hkv in {1, 2, 4, 8}    */
+    int32_t n_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0, 1 <= Hq / Hkv <= 8           */
     int32_t head_dim;    /* d in {64, 128}                                       */
     int64_t max_len;     /* rows allocated per (b, KV head) in k and v, < 2^31   */
     int32_t k;           /* K: support size, 1 <= K <= 2048                      */

@@ -164,6 +164,15 @@ template <typename T, int D> struct RowT {
     static constexpr int kEPV = 16 / (int)sizeof(T);
 };
 
+// Waves per SIMD that the kernels holding a group's G query vectors per lane
+// (G * kNV * 4 registers) are built for: 4 (two 512-thread blocks per CU), or 2
+// (256 registers a lane) where the queries alone would take half of 128.
+template <typename T, int D, int G>
+constexpr int kGroupWaves = G * RowT<T, D>::kNV > 16 ? 2 : 4;
+// The same for k_dense, whose lanes also hold G value accumulators of kEPV floats.
+template <typename T, int D, int G>
+constexpr int kDenseWaves = G * (4 * RowT<T, D>::kNV + RowT<T, D>::kEPV) > 96 ? 2 : 4;
+
 template <typename T> struct Dot;
 template <> struct Dot<uint16_t> {
     // 8 bf16 products accumulated in fp32 with v_dot2_f32_bf16.
@@ -390,13 +399,16 @@ __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint3
 {
     using R = RowT<T, D>;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
-    const int bh0 = b * a.Hq + g * G;
+    const int bh0 = b * a.Hq + g * a.G;
     if (a.mode == MODE_SELECT && row0 == 0 && tid == 0) atomicAdd(&w.stats[STAT_SCANS], 1ull);
     const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
+    // G >= a.G: the heads past a.G pad the group (they read head 0's query and are
+    // never in exmask)
     uint4 qv[G][R::kNV];
 #pragma unroll
     for (int j = 0; j < G; ++j) {
-        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)(bh0 + j) * a.q_head_stride);
+        const int hj = j < a.G ? j : 0;
+        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)(bh0 + hj) * a.q_head_stride);
 #pragma unroll
         for (int s = 0; s < R::kNV; ++s) qv[j][s] = qr[s * 4 + p];
     }
@@ -487,7 +499,7 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
         }
     };
     if constexpr (!kSelect) {
-        do_span(NG, [](int e, int &gi, uint32_t &m) { gi = e; m = (1u << G) - 1u; });
+        do_span(NG, [&](int e, int &gi, uint32_t &m) { gi = e; m = (1u << a.G) - 1u; });
     } else {
         __shared__ uint32_t s_reuse[kMaxHeads / 32];
         __shared__ uint32_t s_local[kLocalGroups];   // group * 256 + exact-head mask
@@ -504,11 +516,11 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
         __syncthreads();
         auto mask_of = [&](int gi) {
             uint32_t m = 0u;
-            const int head0 = (gi / a.Hkv) * a.Hq + (gi % a.Hkv) * G;
+            const int head0 = (gi / a.Hkv) * a.Hq + (gi % a.Hkv) * a.G;
 #pragma unroll
             for (int j = 0; j < G; ++j) {
                 const int head = head0 + j;
-                if (!((s_reuse[head >> 5] >> (head & 31)) & 1u)) m |= 1u << j;
+                if (j < a.G && !((s_reuse[head >> 5] >> (head & 31)) & 1u)) m |= 1u << j;
             }
             return m;
         };
@@ -822,7 +834,7 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
 // every head is exact and the grid holds scan blocks only.  Dynamic LDS:
 // max(score_scan_lds(G), score_range_lds(merge candidates)) bytes.
 template <typename T, int D, int G, bool kSelect>
-__global__ __launch_bounds__(kScoreThreads, 4) void k_score(StepArgs a, Ws w, Geometry geo)
+__global__ __launch_bounds__(kScoreThreads, (kGroupWaves<T, D, G>)) void k_score(StepArgs a, Ws w, Geometry geo)
 {
     extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
     if (kSelect && (int)blockIdx.x < geo.cand_blocks)
@@ -1487,7 +1499,7 @@ __global__ __launch_bounds__(kPfThreads) void k_pf_score(StepArgs a, Ws w, Geome
 // weights exp(s - m), their sum l and the weighted sum o of the value rows.
 // (o, m, l) go to dense_part; k_dense_merge rescales and adds the chunks.
 template <typename T, int D, int G>
-__global__ __launch_bounds__(kDenseThreads, 4) void k_dense(StepArgs a, Ws w)
+__global__ __launch_bounds__(kDenseThreads, (kDenseWaves<T, D, G>)) void k_dense(StepArgs a, Ws w)
 {
     using R = RowT<T, D>;
     constexpr int NT = kDenseThreads, NW = NT / 64;
@@ -1502,7 +1514,7 @@ __global__ __launch_bounds__(kDenseThreads, 4) void k_dense(StepArgs a, Ws w)
     const int nch = (int)((a.len + kDenseRows - 1) / kDenseRows);
     const int c = blockIdx.x % nch, bg = blockIdx.x / nch;
     const int b = bg / a.Hkv, g = bg % a.Hkv;
-    const int bh0 = b * a.Hq + g * G;
+    const int bh0 = b * a.Hq + g * a.G;      // heads past a.G pad the group
     const int64_t r0 = (int64_t)c * kDenseRows;
     const int nrow = (int)(a.len - r0 < kDenseRows ? a.len - r0 : kDenseRows);
     const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
@@ -1511,7 +1523,8 @@ __global__ __launch_bounds__(kDenseThreads, 4) void k_dense(StepArgs a, Ws w)
     uint4 qv[G][R::kNV];
 #pragma unroll
     for (int j = 0; j < G; ++j) {
-        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)(bh0 + j) * a.q_head_stride);
+        const int hj = j < a.G ? j : 0;
+        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)(bh0 + hj) * a.q_head_stride);
 #pragma unroll
         for (int v = 0; v < R::kNV; ++v) qv[j][v] = qr[v * 4 + p];
     }
@@ -1622,7 +1635,7 @@ __global__ __launch_bounds__(kDenseThreads, 4) void k_dense(StepArgs a, Ws w)
 #pragma unroll
             for (int e = 0; e < EPV; ++e) s_o[wave][j][vl * EPV + e] = acc[j][e];
     __syncthreads();
-    for (int i = tid; i < G * D; i += NT) {
+    for (int i = tid; i < a.G * D; i += NT) {
         const int j = i / D, e = i % D;
         float o = 0.0f;
 #pragma unroll
@@ -1709,8 +1722,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_dense_merge(StepArgs a, Ws w)
 
 bool shape_supported(int dtype, int d, int g)
 {
-    return (dtype == 0 || dtype == 1) && (d == 64 || d == 128) &&
-           (g == 1 || g == 2 || g == 4 || g == 8);
+    return (dtype == 0 || dtype == 1) && (d == 64 || d == 128) && g >= 1 && g <= 8;
 }
 
 template <typename T, int D>
@@ -1743,13 +1755,15 @@ static void final_desc(const StepArgs &a, KernelDesc *k)
                     dim3(kFinalThreads), 0u, 2};
 }
 
+// Group sizes run on the build for the next power of two (1, 2, 4 or 8); the
+// extra heads pad the group.
 template <typename T, int D>
 static void score_g(const StepArgs &a, const Geometry &geo, KernelDesc *k)
 {
     switch (a.G) {
     case 1: return score_desc<T, D, 1>(a, geo, k);
     case 2: return score_desc<T, D, 2>(a, geo, k);
-    case 4: return score_desc<T, D, 4>(a, geo, k);
+    case 3: case 4: return score_desc<T, D, 4>(a, geo, k);
     default: return score_desc<T, D, 8>(a, geo, k);
     }
 }
@@ -1762,7 +1776,7 @@ static void dense_g(const StepArgs &a, KernelDesc *k)
     switch (a.G) {
     case 1: f = (const void *)&k_dense<T, D, 1>; break;
     case 2: f = (const void *)&k_dense<T, D, 2>; break;
-    case 4: f = (const void *)&k_dense<T, D, 4>; break;
+    case 3: case 4: f = (const void *)&k_dense<T, D, 4>; break;
     default: f = (const void *)&k_dense<T, D, 8>; break;
     }
     *k = KernelDesc{f, dim3(blocks), dim3(kDenseThreads), 0u, 2};

@@ -77,6 +77,10 @@ WORKLOADS = {
     # C = W = 32, R = 4, tau = 0.85, T_r = 128).
     "128k_paper": Workload("128k_paper", 1, 32, 8, 128, "bf16", 131072, 256, 512, 32, 4, 32,
                            0.85, 128, 256, 0.9, 0.05),
+    # The layer layout of the paper's main model (Qwen2.5-7B: 28 query heads on 4
+    # KV heads, d = 128) at 128K with the default selector settings.
+    "128k_28x4_paper": Workload("128k_28x4_paper", 1, 28, 4, 128, "bf16", 131072, 256, 512, 32,
+                                4, 32, 0.85, 128, 256, 0.9, 0.05),
     # Fallback-heavy: four sequences at 64K, frequent jumps, tau = 0.9.
     "stress": Workload("stress", 4, 32, 8, 128, "bf16", 65536, 256, 1024, 512, 8, 256, 0.9, 16,
                        256, 0.9, 0.3),

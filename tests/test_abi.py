@@ -56,7 +56,7 @@ def _cfg(**kw):
     (dict(cache_cap=-1), -1), (dict(r=0), -1), (dict(window=-1), -1), (dict(refresh=-1), -1),
     (dict(tau=float("nan")), -1), (dict(tau=float("inf")), -1), (dict(dtype=7), -1),
     (dict(retrieval=2), -1), (dict(retrieval=-1), -1),
-    (dict(head_dim=96), -2), (dict(n_q_heads=24, n_kv_heads=8), -2), (dict(k=4096), -2),
+    (dict(head_dim=96), -2), (dict(n_q_heads=32, n_kv_heads=2), -2), (dict(k=4096), -2),
     (dict(r=64), -2), (dict(cache_cap=8192), -2),
 ])
 def test_create_rejects_bad_config(lib, bad, code):

@@ -142,14 +142,24 @@ SHAPES = [
     # the largest K
     ("bf16_k2048", dict(n_q_heads=2, n_kv_heads=1, prompt_len=9000, steps=16, k=2048,
                         cache_cap=16, r=2, window=128, refresh=8, n_centers=8)),
+    # group sizes that are not powers of two: 7 (the 28 / 4 layout of the paper's
+    # Qwen2.5-7B), 3 over two sequences, 5 in fp32
+    ("bf16_d128_g7", dict(n_q_heads=14, n_kv_heads=2, prompt_len=5000, steps=40, k=128,
+                          cache_cap=32, r=4, window=64, refresh=16, n_centers=16)),
+    ("bf16_d64_g3_b2", dict(batch=2, n_q_heads=6, n_kv_heads=2, head_dim=64, prompt_len=3000,
+                            steps=32, k=64, cache_cap=24, r=3, window=32, refresh=10,
+                            n_centers=12)),
+    ("f32_d64_g5", dict(dtype="f32", n_q_heads=10, n_kv_heads=2, head_dim=64, prompt_len=2500,
+                        steps=32, k=48, cache_cap=24, r=4, window=32, refresh=12, n_centers=12)),
 ]
 
 
 @pytest.mark.parametrize("label, change", SHAPES, ids=[s_[0] for s_ in SHAPES])
 def test_decode_lockstep_shapes(label, change):
     """d = 64 with eight query heads per KV head, one query head per KV head over
-    two sequences, fp32 at d = 128, the largest cache with the largest R, and the
-    largest K: all heads, all steps, in lock-step from the oracle's prefill state."""
+    two sequences, fp32 at d = 128, the largest cache with the largest R, the
+    largest K, and groups of 7, 3 and 5 query heads: all heads, all steps, in
+    lock-step from the oracle's prefill state."""
     w = WORKLOADS["16k"].with_(**change)
     print(f"decode lock-step {label}", flush=True)
     inp = make_inputs(w)
@@ -175,7 +185,7 @@ def test_decode_lockstep_16k_two_groups():
     assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * w.steps
 
 
-@pytest.mark.parametrize("name", ["32k", "128k", "128k_paper", "stress"])
+@pytest.mark.parametrize("name", ["32k", "128k", "128k_paper", "128k_28x4_paper", "stress"])
 def test_decode_full_size_sampled(name):
     """Full-size layer shapes: the cache starts from the prompt-tail queries with
     seeded supports (no prefill), and 3 steps run in lock-step; KV group 0 of the

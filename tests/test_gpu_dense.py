@@ -24,6 +24,10 @@ CASES = [
     ("bf16", 64, 1, 4, 4, 5000),
     ("bf16", 128, 1, 4, 1, 1),
     ("bf16", 128, 1, 8, 4, 1024),
+    # group sizes that are not powers of two (padded groups)
+    ("bf16", 128, 1, 28, 4, 9000),
+    ("bf16", 64, 2, 6, 2, 4097),
+    ("f32", 128, 1, 10, 2, 3000),
 ]
 
 

@@ -115,14 +115,19 @@ SHAPES = [
                             cache_cap=20, n_centers=32), 7),
     ("k_above_len", dict(n_q_heads=4, n_kv_heads=2, prompt_len=300, k=512, cache_cap=30,
                          n_centers=8), 0),
+    # groups of 7 and 6 query heads (virtual queries u * G + j across tile edges)
+    ("g7_d128", dict(n_q_heads=7, n_kv_heads=1, prompt_len=3500, k=96, cache_cap=36,
+                     n_centers=16), 0),
+    ("g6_d64_b2", dict(batch=2, n_q_heads=12, n_kv_heads=2, head_dim=64, prompt_len=2600,
+                       k=64, cache_cap=20, n_centers=12), 3),
 ]
 
 
 @pytest.mark.parametrize("label,change,extra", SHAPES, ids=[s[0] for s in SHAPES])
 def test_prefill_batched_shapes(label, change, extra):
     """Group sizes 8 and 1, d = 64, batch 2, more prompt-tail queries than cache
-    slots (the early ones are overwritten), and K above the causal length (the
-    whole prefix is the support): all heads, all positions."""
+    slots (the early ones are overwritten), K above the causal length (the whole
+    prefix is the support), and groups of 7 and 6: all heads, all positions."""
     w = WORKLOADS["16k"].with_(**change)
     w = w.with_(cache_cap=w.cache_cap + extra)   # generate the extra positions too
     print(f"batched prefill {label}", flush=True)
