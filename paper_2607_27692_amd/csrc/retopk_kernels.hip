@@ -164,11 +164,11 @@ template <typename T, int D> struct RowT {
     static constexpr int kEPV = 16 / (int)sizeof(T);
 };
 
-// Waves per SIMD that the kernels holding a group's G query vectors per lane
-// (G * kNV * 4 registers) are built for: 4 (two 512-thread blocks per CU), or 2
-// (256 registers a lane) where the queries alone would take half of 128.
+// Waves per SIMD that k_score is built for: 4 (two 512-thread blocks per CU), or
+// 2 (256 registers a lane) where the group's query vectors alone would take half
+// of 128 registers (G * kNV * 4 in the quad layout, half that in the octet one).
 template <typename T, int D, int G>
-constexpr int kGroupWaves = G * RowT<T, D>::kNV > 16 ? 2 : 4;
+constexpr int kGroupWaves = (G == 8 ? 2 : 4) * G * RowT<T, D>::kNV > 64 ? 2 : 4;
 // The same for k_dense, whose lanes also hold G value accumulators of kEPV floats.
 template <typename T, int D, int G>
 constexpr int kDenseWaves = G * (4 * RowT<T, D>::kNV + RowT<T, D>::kEPV) > 96 ? 2 : 4;
@@ -247,6 +247,23 @@ __device__ __forceinline__ void group_scores(const float (&acc)[G], int p, float
         s_lo = quad_transpose_sum(acc[0], acc[1], acc[2], acc[3], p);
         s_hi = quad_transpose_sum(acc[4], acc[5], acc[6], acc[7], p);
     }
+}
+
+// Reduce-scatter inside an octet of lanes (8 lanes per row, one per head of an
+// 8-head group): lane o holds partial sums of the 8 dot products and returns the
+// full (8-lane) sum of dot product o.  Three butterfly steps, as in
+// quad_transpose_sum.
+__device__ __forceinline__ float octet_transpose_sum(const float (&acc)[8], int o)
+{
+    const bool b2 = (o & 4) != 0, b1 = (o & 2) != 0, b0 = (o & 1) != 0;
+    float h4[4], h2[2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)   // heads (o & 4) + i
+        h4[i] = (b2 ? acc[i + 4] : acc[i]) + __shfl_xor(b2 ? acc[i] : acc[i + 4], 4);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)   // heads (o & 6) + i
+        h2[i] = (b1 ? h4[i + 2] : h4[i]) + dpp_f32<kQuadXor2>(b1 ? h4[i] : h4[i + 2]);
+    return (b0 ? h2[1] : h2[0]) + dpp_f32<kQuadXor1>(b0 ? h2[0] : h2[1]);   // head o
 }
 
 // ---------------------------------------------------------------------------
@@ -390,6 +407,79 @@ __host__ __device__ constexpr int score_range_lds(int n_merge)
 }
 constexpr int kLocalGroups = 512;   // exact KV groups one scan block's rows can touch
 
+// scan_segment for the 8-head build (groups of 5 to 8): a key row is split over
+// the 8 lanes of an octet, lane o loading 16-byte vectors s * 8 + o, so that each
+// lane holds half the query registers of the quad layout, and after the octet
+// reduce-scatter lane o owns head o's score.  64 rows per pass of the block, 4
+// passes (256 rows) per iteration, loaded from clamped (in-bounds) rows.
+template <typename T, int D>
+__device__ void scan_segment_octet(const StepArgs &a, const Ws &w, int b, int g, uint32_t exmask,
+                                   int64_t row0, int64_t row1, uint32_t *s_hist)
+{
+    constexpr int G = 8;
+    constexpr int NV = RowT<T, D>::kBytes / 128;          // vectors per lane per row
+    constexpr int RPP = kScoreThreads / 8;                // rows per pass
+    constexpr int UP = 2 * kScanRowsPerIter / RPP;        // passes per iteration
+    static_assert(NV >= 1 && UP * RPP == 2 * kScanRowsPerIter, "octet row geometry");
+    const int tid = threadIdx.x, o = tid & 7, rr = tid >> 3;
+    const int bh0 = b * a.Hq + g * a.G;
+    if (a.mode == MODE_SELECT && row0 == 0 && tid == 0) atomicAdd(&w.stats[STAT_SCANS], 1ull);
+    const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
+    uint4 qv[G][NV];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        const int hj = j < a.G ? j : 0;   // heads past a.G pad the group
+        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)(bh0 + hj) * a.q_head_stride);
+#pragma unroll
+        for (int s = 0; s < NV; ++s) qv[j][s] = qr[s * 8 + o];
+    }
+    const bool keep = o < a.G && ((exmask >> o) & 1u);   // head o is exact
+    uint4 kv[UP][NV];
+    int row[UP];                          // rows < len < 2^31
+    auto load = [&](int64_t base) {
+#pragma unroll
+        for (int u = 0; u < UP; ++u) {
+            row[u] = (int)base + u * RPP + rr;
+            const uint4 *rp = (const uint4 *)(kbase + (row[u] < row1 ? (int64_t)row[u] : row0) * D);
+#pragma unroll
+            for (int s = 0; s < NV; ++s) kv[u][s] = rp[s * 8 + o];
+        }
+    };
+    load(row0);   // the first rows are in flight while the histogram is cleared
+    __syncthreads();   // the previous segment's histogram flush is done
+    for (int i = tid; i < G * kHistBins; i += kScoreThreads) s_hist[i] = 0u;
+    __syncthreads();
+
+    for (int64_t base = row0; base < row1;) {
+#pragma unroll
+        for (int u = 0; u < UP; ++u) {
+            float acc[G];
+#pragma unroll
+            for (int j = 0; j < G; ++j) {
+                float s0 = 0.0f;
+#pragma unroll
+                for (int s = 0; s < NV; ++s) s0 = Dot<T>::f(kv[u][s], qv[j][s], s0);
+                acc[j] = s0;
+            }
+            const float sc = octet_transpose_sum(acc, o) * a.inv_sqrt_d;
+            if (keep && row[u] < row1) {
+                w.scores[(int64_t)(bh0 + o) * a.row_stride + row[u]] = sc;
+                atomicAdd(&s_hist[o * kHistBins + (ord_key(sc) >> kHistShift)], 1u);
+            }
+        }
+        base += UP * RPP;
+        if (base < row1) load(base);
+    }
+    __syncthreads();
+    for (int i = tid; i < G * kHistBins; i += kScoreThreads) {
+        const int j = i / kHistBins;
+        if ((exmask >> j) & 1u) {
+            const uint32_t c = s_hist[i];
+            if (c) atomicAdd(&w.hist[(int64_t)(bh0 + j) * kHistBins + (i % kHistBins)], c);
+        }
+    }
+}
+
 // One contiguous segment [row0, row1) of the rows of KV group (b, g): scores of
 // the group's exact heads (bits of exmask), written to `scores` and counted in
 // each head's histogram.
@@ -397,6 +487,10 @@ template <typename T, int D, int G>
 __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint32_t exmask,
                              int64_t row0, int64_t row1, uint32_t *s_hist)
 {
+    if constexpr (G == 8) {
+        scan_segment_octet<T, D>(a, w, b, g, exmask, row0, row1, s_hist);
+        return;
+    }
     using R = RowT<T, D>;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
     const int bh0 = b * a.Hq + g * a.G;
