@@ -1013,6 +1013,7 @@ struct FinalSmem {
     float qbar[D];
     double red64[NT / 64];
     uint32_t redu[NT / 64];
+    uint32_t wcnt[NT / 64];         // per-wave counts of the ordered compaction
     uint64_t tie[kTieMax];          // entries of the bin that holds the K-th largest
     unsigned long long rmax, rmin;
     uint64_t thr;
@@ -1126,21 +1127,32 @@ __device__ bool value_threshold(const uint64_t *ent, int n, int K, FinalSmem<D, 
     const float range = smax - smin;
     if (!(range > 0.0f) || !(range < 3.0e38f)) return false;   // block-uniform
     const float scale = (float)(kHistBins - 1) / range;
-    for (int j = tid; j < n; j += NT) {
-        const float sc = key_score(rank_key(ent[j]));
-        const int bin = min((int)((sc - smin) * scale), kHistBins - 1);
-        atomicAdd(&sm.hist[bin], 1u);
+    auto bin_of = [&](uint64_t e) {
+        const float sc = key_score(rank_key(e));
+        return min((int)((sc - smin) * scale), kHistBins - 1);
+    };
+    // four entries per thread in flight (LDS reads issued before their use)
+    for (int j0 = tid; j0 < n; j0 += 4 * NT) {
+        uint64_t e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) e[u] = ent[j0 + u * NT < n ? j0 + u * NT : j0];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (j0 + u * NT < n) atomicAdd(&sm.hist[bin_of(e[u])], 1u);
     }
     __syncthreads();
     find_bin<D, NT>(sm, kHistBins, (uint32_t)K);
     const uint32_t bstar = sm.found_digit, cnt = sm.found_cnt;
     const uint32_t k_rem = (uint32_t)K - sm.found_above;
     if (cnt > (uint32_t)kTieMax) return false;
-    for (int j = tid; j < n; j += NT) {
-        const uint64_t e = ent[j];
-        const float sc = key_score(rank_key(e));
-        const int bin = min((int)((sc - smin) * scale), kHistBins - 1);
-        if ((uint32_t)bin == bstar) sm.tie[atomicAdd(&sm.n_tie, 1u)] = e;
+    for (int j0 = tid; j0 < n; j0 += 4 * NT) {
+        uint64_t e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) e[u] = ent[j0 + u * NT < n ? j0 + u * NT : j0];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (j0 + u * NT < n && (uint32_t)bin_of(e[u]) == bstar)
+                sm.tie[atomicAdd(&sm.n_tie, 1u)] = e[u];
     }
     __syncthreads();
     if (tid < 64) {
@@ -1353,17 +1365,48 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     }
     const int kn = rg.n < a.K ? rg.n : a.K;
     {
-        const int ept = (rg.n + NT - 1) / NT;
-        const int j0 = tid * ept < rg.n ? tid * ept : rg.n;
-        const int j1 = j0 + ept < rg.n ? j0 + ept : rg.n;
-        uint32_t mine = 0;
-        for (int j = j0; j < j1; ++j) mine += rg.get(j) >= thr ? 1u : 0u;
-        uint32_t total;
-        uint32_t pos = block_excl_scan<NT>(mine, sm.redu, &total);
-        for (int j = j0; j < j1; ++j) {
-            const uint64_t e = rg.get(j);
-            if (e >= thr && pos < (uint32_t)kMaxK)
-                sm.sel[pos++] = ((uint64_t)rank_index(e) << 32) | rank_key(e);
+        // Wave w compacts entries [w * per, (w + 1) * per) in order, 64 consecutive
+        // entries per ballot (conflict-free LDS reads): one pass counts its
+        // selected entries, a second writes them after those of the waves before.
+        const int per = ((rg.n + NW - 1) / NW + 63) & ~63;
+        const int jb = wave * per, je = min(jb + per, rg.n);
+        const uint64_t below = (1ull << lane) - 1ull;
+        const uint64_t *stg = rg.staged;
+        // staged entries are read from LDS directly (no per-entry branch)
+        auto entry = [&](int j) { return stg ? stg[j] : rg.get(j); };
+        uint32_t cnt = 0u;
+        for (int j0 = jb; j0 < je; j0 += 4 * 64) {
+            uint64_t e[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int j = j0 + u * 64 + lane;
+                e[u] = entry(j < je ? j : jb);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                cnt += (uint32_t)__popcll(__ballot(j0 + u * 64 + lane < je && e[u] >= thr));
+        }
+        if (lane == 0) sm.wcnt[wave] = cnt;
+        __syncthreads();
+        uint32_t pos = 0u;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) pos += ww < wave ? sm.wcnt[ww] : 0u;
+        for (int j0 = jb; j0 < je; j0 += 4 * 64) {
+            uint64_t e[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int j = j0 + u * 64 + lane;
+                e[u] = entry(j < je ? j : jb);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool s = j0 + u * 64 + lane < je && e[u] >= thr;
+                const uint64_t bal = __ballot(s);
+                const uint32_t at = pos + (uint32_t)__popcll(bal & below);
+                if (s && at < (uint32_t)kMaxK)
+                    sm.sel[at] = ((uint64_t)rank_index(e[u]) << 32) | rank_key(e[u]);
+                pos += (uint32_t)__popcll(bal);
+            }
         }
         __syncthreads();
     }
