@@ -208,19 +208,24 @@ def test_one_hot_values_expose_weights(oracle_lib):
         assert abs(math.log(w[chosen[a]] / w[chosen[0]]) - (s[a] - s[0])) < 1e-5
 
 
-def test_gqa_head_mapping(oracle_lib):
-    """Query head h reads KV head h // (Hq / Hkv): zero keys and constant values in KV
-    head 1 make heads 2 and 3 return that constant."""
+@pytest.mark.parametrize("Hq, Hkv", [(4, 2), (14, 2), (9, 3)])
+def test_gqa_head_mapping(oracle_lib, Hq, Hkv):
+    """Query head h reads KV head h // (Hq / Hkv): zero keys and constant values in the
+    last KV head make exactly its G query heads return that constant (G = 2, and the
+    group sizes 7 and 3 that are not powers of two)."""
     rng = np.random.default_rng(5)
-    B, Hq, Hkv, d, L = 1, 4, 2, 8, 20
+    B, d, L = 1, 8, 20
+    G = Hq // Hkv
     q, k, v = _rand_case(rng, B, Hq, Hkv, d, L)
-    k[0, 1] = 0
-    v[0, 1] = 3.25
+    k[0, Hkv - 1] = 0
+    v[0, Hkv - 1] = 3.25
     p = _params(batch=B, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, max_len=L, k=5)
     out, sel, _ = O.exact(p, q, k, v, L)
-    np.testing.assert_array_equal(out[0, 2:], 3.25)
-    assert sel[0, 2].tolist() == [0, 1, 2, 3, 4]
-    assert not np.allclose(out[0, :2], 3.25)
+    np.testing.assert_array_equal(out[0, Hq - G:], 3.25)
+    for h in range(Hq - G, Hq):
+        assert sel[0, h].tolist() == [0, 1, 2, 3, 4]
+    for h in range(Hq - G):
+        assert not np.allclose(out[0, h], 3.25)
 
 
 # ---------------------------------------------------------------------------
