@@ -467,7 +467,19 @@ def cpu_baseline(w, inp, seconds: float):
             "sample": (f"oracle (plain C, 1 thread) on the {len(heads)} query heads of KV group "
                        f"0, {n_st} ReTopK steps from a seeded cache state and {n_ex} Exact "
                        f"Top-K steps, scaled x{scale:g} to all heads"),
-            "cpu": platform.processor() or platform.machine()}
+            "cpu": _cpu_model(), "host_cores": os.cpu_count()}
+
+
+def _cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo where there is one)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 # ---- fidelity diagnostics ------------------------------------------------------
