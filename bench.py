@@ -367,6 +367,7 @@ def main():
         "exact_us_median": round(float(np.median(e_ms)) * 1e3, 2),
         "fallback_rate": round(fallback / head_steps, 4) if head_steps else None,
         "refresh_share": round(refresh / head_steps, 4) if head_steps else None,
+        "cold_head_steps": int(st["cold"]),
         "mean_candidates": round(cand_sum / reuse, 1) if reuse else None,
         "max_candidates": st["cand_max"],
         "wall_s_exact": round(e_wall, 4),
