@@ -77,11 +77,16 @@ def test_prefill_batched_16k():
     print(tally, flush=True)
 
 
-def test_prefill_batched_128k_sampled():
-    """128K, 512 positions in several launches: positions on both sides of the
-    launch boundaries and at the ends, KV groups 0 and 7, against the oracle's
-    Exact Top-K of each query over its causal prefix."""
-    w = WORKLOADS["128k"]
+@pytest.mark.parametrize("name, positions", [
+    ("128k", (0, 1, 40, 41, 42, 81, 82, 255, 256, 492, 493, 510, 511)),
+    ("128k_28x4_paper", (0, 1, 15, 16, 30, 31)),
+])
+def test_prefill_batched_128k_sampled(name, positions):
+    """128K: 512 positions in several launches (positions on both sides of the
+    launch boundaries and at the ends), and the 28 / 4 head layout with 32 slots;
+    the first and last KV groups, against the oracle's Exact Top-K of each query
+    over its causal prefix."""
+    w = WORKLOADS[name]
     print(f"batched prefill {w.name}", flush=True)
     inp = make_inputs(w)
     p = params_of(w)
@@ -91,7 +96,7 @@ def test_prefill_batched_128k_sampled():
     assert gst["n_inserted"] == n
     qt, kf, vf = inp.q_tail, inp.k, inp.v      # widened once
     tally = Tally()
-    for u in (0, 1, 40, 41, 42, 81, 82, 255, 256, 492, 493, 510, 511):
+    for u in positions:
         length = w.prompt_len - n + u + 1
         _, osel, _ = O.exact(p, qt[:, :, u], kf, vf, length, head_mask=mask)
         for bh in heads:
