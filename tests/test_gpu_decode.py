@@ -262,10 +262,14 @@ def test_prefill_and_free_running_trajectory_small():
     assert stats["refresh"] == (w.steps - 1) // w.refresh
 
 
-def test_determinism_16k():
-    """Two GPU runs of the same 16K trajectory (prefill + 32 steps) are bitwise equal."""
+@pytest.mark.parametrize("layout", ["32x8", "28x4"])
+def test_determinism_16k(layout):
+    """Two GPU runs of the same 16K trajectory (prefill + 32 steps) are bitwise equal,
+    for 32 query heads on 8 KV heads and for 28 on 4 (groups of 7)."""
     w = WORKLOADS["16k"]
-    print(f"determinism {w.name}", flush=True)
+    if layout == "28x4":
+        w = w.with_(n_q_heads=28, n_kv_heads=4)
+    print(f"determinism {w.name} {layout}", flush=True)
     inp = make_inputs(w)
     dev = _dev_inputs(inp)
     a = _free_run(w, inp, dev, 32)
