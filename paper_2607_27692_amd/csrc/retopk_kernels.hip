@@ -169,9 +169,12 @@ template <typename T, int D> struct RowT {
 // of 128 registers (G * kNV * 4 in the quad layout, half that in the octet one).
 template <typename T, int D, int G>
 constexpr int kGroupWaves = (G == 8 ? 2 : 4) * G * RowT<T, D>::kNV > 64 ? 2 : 4;
-// The same for k_dense, whose lanes also hold G value accumulators of kEPV floats.
+// The same for k_dense, whose lanes also hold G value accumulators of kEPV floats
+// (the 8-head build takes its scores in the octet layout, its queries dead by
+// the time the accumulators live).
 template <typename T, int D, int G>
-constexpr int kDenseWaves = G * (4 * RowT<T, D>::kNV + RowT<T, D>::kEPV) > 96 ? 2 : 4;
+constexpr int kDenseWaves = G == 8 ? (16 * RowT<T, D>::kNV > 64 ? 2 : 4)
+                                   : (G * (4 * RowT<T, D>::kNV + RowT<T, D>::kEPV) > 96 ? 2 : 4);
 
 template <typename T> struct Dot;
 template <> struct Dot<uint16_t> {
@@ -1646,6 +1649,7 @@ __global__ __launch_bounds__(kDenseThreads, (kDenseWaves<T, D, G>)) void k_dense
     static_assert(VL >= 1 && VL <= 64 && 64 % VL == 0, "value row geometry");
     __shared__ float s_sc[G][kDenseRows];
     __shared__ float s_red[NW][G];
+    __shared__ float s_ml[2][G];            // each head's chunk maximum and weight sum
     __shared__ float s_o[NW][G][D];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
     const int nch = (int)((a.len + kDenseRows - 1) / kDenseRows);
@@ -1657,6 +1661,44 @@ __global__ __launch_bounds__(kDenseThreads, (kDenseWaves<T, D, G>)) void k_dense
     const T *kbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
     const T *vbase = (const T *)a.v + ((int64_t)b * a.Hkv + g) * a.max_len * D;
 
+    if constexpr (G == 8) {
+        // scores (Eq. 4) of the chunk's rows in the octet layout of
+        // scan_segment_octet: lane o owns head o's score of its row
+        constexpr int NV = R::kBytes / 128, RPP = NT / 8, UP = 2 * kScanRowsPerIter / RPP;
+        const int o = tid & 7, rr = tid >> 3;
+        uint4 qv[G][NV];
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int hj = j < a.G ? j : 0;
+            const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)(bh0 + hj) * a.q_head_stride);
+#pragma unroll
+            for (int v = 0; v < NV; ++v) qv[j][v] = qr[v * 8 + o];
+        }
+        for (int base = 0; base < nrow; base += UP * RPP) {
+            uint4 kv[UP][NV];
+            int row[UP];
+#pragma unroll
+            for (int u = 0; u < UP; ++u) {
+                row[u] = base + u * RPP + rr;
+                const uint4 *rp = (const uint4 *)(kbase + (r0 + (row[u] < nrow ? row[u] : 0)) * D);
+#pragma unroll
+                for (int v = 0; v < NV; ++v) kv[u][v] = rp[v * 8 + o];
+            }
+#pragma unroll
+            for (int u = 0; u < UP; ++u) {
+                float acc[G];
+#pragma unroll
+                for (int j = 0; j < G; ++j) {
+                    float s0 = 0.0f;
+#pragma unroll
+                    for (int v = 0; v < NV; ++v) s0 = Dot<T>::f(kv[u][v], qv[j][v], s0);
+                    acc[j] = s0;
+                }
+                const float sc = octet_transpose_sum(acc, o) * a.inv_sqrt_d;
+                if (row[u] < nrow) s_sc[o][row[u]] = sc;
+            }
+        }
+    } else {
     uint4 qv[G][R::kNV];
 #pragma unroll
     for (int j = 0; j < G; ++j) {
@@ -1698,6 +1740,7 @@ __global__ __launch_bounds__(kDenseThreads, (kDenseWaves<T, D, G>)) void k_dense
             }
         }
     }
+    }
     __syncthreads();
     // per head: chunk maximum, then weights exp(s - m) in place and their sum
     float m[G], l[G];
@@ -1736,23 +1779,31 @@ __global__ __launch_bounds__(kDenseThreads, (kDenseWaves<T, D, G>)) void k_dense
 #pragma unroll
         for (int i = 0; i < NW; ++i) l[j] += s_red[i][j];
     }
+    if (tid == 0) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            s_ml[0][j] = m[j];
+            s_ml[1][j] = l[j];
+        }
+    }
     // Eq. 12 over the chunk: VL lanes per value row, each holding EPV elements
-    // for every head; rows spread over the waves.
+    // for every head; rows spread over the waves (VU rows per lane in flight).
+    constexpr int VU = G == 8 ? 2 : 4;
     const int sub = lane / VL, vl = lane % VL;
     float acc[G][EPV];
 #pragma unroll
     for (int j = 0; j < G; ++j)
 #pragma unroll
         for (int e = 0; e < EPV; ++e) acc[j][e] = 0.0f;
-    for (int t0 = wave * VR; t0 < nrow; t0 += NW * VR * 4) {
-        uint4 raw[4];
+    for (int t0 = wave * VR; t0 < nrow; t0 += NW * VR * VU) {
+        uint4 raw[VU];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < VU; ++u) {
             const int t = t0 + u * NW * VR + sub;
             raw[u] = ((const uint4 *)(vbase + (r0 + (t < nrow ? t : 0)) * D))[vl];
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < VU; ++u) {
             const int t = t0 + u * NW * VR + sub;
             if (t < nrow) {
 #pragma unroll
@@ -1780,8 +1831,8 @@ __global__ __launch_bounds__(kDenseThreads, (kDenseWaves<T, D, G>)) void k_dense
         float *dst = w.dense_part + ((int64_t)(bh0 + j) * a.n_dense + c) * (D + 2);
         dst[e] = o;
         if (e == 0) {
-            dst[D] = m[j];
-            dst[D + 1] = l[j];
+            dst[D] = s_ml[0][j];
+            dst[D + 1] = s_ml[1][j];
         }
     }
 }
