@@ -76,6 +76,7 @@ template <> __device__ __forceinline__ double elem_f64<uint16_t>(const uint16_t 
 
 constexpr int kQuadXor1 = 0xB1;   // quad_perm:[1,0,3,2]
 constexpr int kQuadXor2 = 0x4E;   // quad_perm:[2,3,0,1]
+constexpr int kHalfMirror = 0x141; // row_half_mirror: lane i <-> 7 - i in each 8 lanes
 
 template <int CTRL> __device__ __forceinline__ float dpp_f32(float x)
 {
@@ -255,14 +256,15 @@ __device__ __forceinline__ void group_scores(const float (&acc)[G], int p, float
 // Reduce-scatter inside an octet of lanes (8 lanes per row, one per head of an
 // 8-head group): lane o holds partial sums of the 8 dot products and returns the
 // full (8-lane) sum of dot product o.  Three butterfly steps, as in
-// quad_transpose_sum.
+// quad_transpose_sum; the first pairs lane o with lane 7 - o (a DPP half-row
+// mirror), whose bit 2 is the opposite of o's, which is all the step needs.
 __device__ __forceinline__ float octet_transpose_sum(const float (&acc)[8], int o)
 {
     const bool b2 = (o & 4) != 0, b1 = (o & 2) != 0, b0 = (o & 1) != 0;
     float h4[4], h2[2];
 #pragma unroll
     for (int i = 0; i < 4; ++i)   // heads (o & 4) + i
-        h4[i] = (b2 ? acc[i + 4] : acc[i]) + __shfl_xor(b2 ? acc[i] : acc[i + 4], 4);
+        h4[i] = (b2 ? acc[i + 4] : acc[i]) + dpp_f32<kHalfMirror>(b2 ? acc[i] : acc[i + 4]);
 #pragma unroll
     for (int i = 0; i < 2; ++i)   // heads (o & 6) + i
         h2[i] = (b1 ? h4[i + 2] : h4[i]) + dpp_f32<kQuadXor2>(b1 ? h4[i] : h4[i + 2]);
