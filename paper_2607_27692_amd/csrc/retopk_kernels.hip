@@ -30,6 +30,8 @@
 namespace retopk {
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
 // Scalar helpers
@@ -169,7 +171,8 @@ template <typename T, int D> struct RowT {
 // 2 (256 registers a lane) where the group's query vectors alone would take half
 // of 128 registers (G * kNV * 4 in the quad layout, half that in the octet one).
 template <typename T, int D, int G>
-constexpr int kGroupWaves = (G == 8 ? 2 : 4) * G * RowT<T, D>::kNV > 64 ? 2 : 4;
+constexpr int kGroupWaves = (G == 8 && sizeof(T) == 2) ? 4
+                            : ((G == 8 ? 2 : 4) * G * RowT<T, D>::kNV > 64 ? 2 : 4);
 // The same for k_dense, whose lanes also hold G value accumulators of kEPV floats
 // (the 8-head build takes its scores in the octet layout, its queries dead by
 // the time the accumulators live).
@@ -485,6 +488,92 @@ __device__ void scan_segment_octet(const StepArgs &a, const Ws &w, int b, int g,
     }
 }
 
+// scan_segment for the bf16 8-head build on the matrix cores: with 8 query
+// vectors per key row the vector-ALU dot products, not HBM, bound the scan, so
+// each wave scores 16-key tiles with v_mfma_f32_16x16x32_bf16 (A: 16 key rows x
+// 32 dims, B: 32 dims x 16 query columns, of which columns 0 .. a.G-1 are the
+// group's heads and the rest repeat head 0; lane l supplies key row and column
+// l % 16 for dims 8 (l / 16) .. + 7 of each 32-dim step and receives keys
+// 4 (l / 16) .. + 3 of column l % 16).  Two tiles per wave, 256 rows per
+// iteration from row0 rounded down to a multiple of 4, so that a lane's four
+// scores are one aligned 16-byte store (rows before row0 are scored, neither
+// stored nor counted); the next rows' loads are issued before the stores.
+template <int D>
+__device__ void scan_segment_mfma(const StepArgs &a, const Ws &w, int b, int g, uint32_t exmask,
+                                  int64_t row0, int64_t row1, uint32_t *s_hist)
+{
+    constexpr int G = 8, KS = D / 32, TW = 2;
+    constexpr int ROWS = (kScoreThreads / 64) * TW * 16;
+    static_assert(D % 32 == 0 && ROWS == 2 * kScanRowsPerIter, "tile geometry");
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 15, kq = lane >> 4;
+    const int bh0 = b * a.Hq + g * a.G;
+    if (a.mode == MODE_SELECT && row0 == 0 && tid == 0) atomicAdd(&w.stats[STAT_SCANS], 1ull);
+    const uint16_t *kbase = (const uint16_t *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
+    bf16x8_t qb[KS];
+    {
+        const int hj = col < a.G ? col : 0;
+        const uint4 *qr = (const uint4 *)((const uint16_t *)a.q + (int64_t)(bh0 + hj) * a.q_head_stride);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qb[ks] = __builtin_bit_cast(bf16x8_t, qr[ks * 4 + kq]);
+    }
+    const bool keep = col < a.G && ((exmask >> col) & 1u);   // column col is an exact head
+    float *srow = w.scores + (int64_t)(bh0 + (keep ? col : 0)) * a.row_stride;
+    uint32_t *hrow = s_hist + col * kHistBins;
+    uint4 kv[TW][KS];
+    auto load = [&](int64_t base) {
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            const int64_t r = base + (wave * TW + t) * 16 + col;
+            const uint4 *rp = (const uint4 *)(kbase + (r < row1 ? r : row0) * D);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) kv[t][ks] = rp[ks * 4 + kq];
+        }
+    };
+    const int64_t start = row0 & ~(int64_t)3;
+    load(start);   // the first rows are in flight while the histogram is cleared
+    __syncthreads();   // the previous segment's histogram flush is done
+    for (int i = tid; i < G * kHistBins; i += kScoreThreads) s_hist[i] = 0u;
+    __syncthreads();
+
+    for (int64_t base = start; base < row1; base += ROWS) {
+        f32x4_t acc[TW];
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            acc[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(bf16x8_t, kv[t][ks]), qb[ks], acc[t], 0, 0, 0);
+        }
+        if (base + ROWS < row1) load(base + ROWS);
+        if (keep) {
+#pragma unroll
+            for (int t = 0; t < TW; ++t) {
+                const int64_t r4 = base + (wave * TW + t) * 16 + 4 * kq;   // a multiple of 4
+                const float sc[4] = {acc[t][0] * a.inv_sqrt_d, acc[t][1] * a.inv_sqrt_d,
+                                     acc[t][2] * a.inv_sqrt_d, acc[t][3] * a.inv_sqrt_d};
+                const bool whole = r4 >= row0 && r4 + 3 < row1;
+                if (whole) *(float4 *)(srow + r4) = make_float4(sc[0], sc[1], sc[2], sc[3]);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (r4 + i >= row0 && r4 + i < row1) {
+                        if (!whole) srow[r4 + i] = sc[i];
+                        atomicAdd(&hrow[ord_key(sc[i]) >> kHistShift], 1u);
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+    for (int i = tid; i < G * kHistBins; i += kScoreThreads) {
+        const int j = i / kHistBins;
+        if ((exmask >> j) & 1u) {
+            const uint32_t c = s_hist[i];
+            if (c) atomicAdd(&w.hist[(int64_t)(bh0 + j) * kHistBins + (i % kHistBins)], c);
+        }
+    }
+}
+
 // One contiguous segment [row0, row1) of the rows of KV group (b, g): scores of
 // the group's exact heads (bits of exmask), written to `scores` and counted in
 // each head's histogram.
@@ -493,7 +582,10 @@ __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint3
                              int64_t row0, int64_t row1, uint32_t *s_hist)
 {
     if constexpr (G == 8) {
-        scan_segment_octet<T, D>(a, w, b, g, exmask, row0, row1, s_hist);
+        if constexpr (sizeof(T) == 2)
+            scan_segment_mfma<D>(a, w, b, g, exmask, row0, row1, s_hist);
+        else
+            scan_segment_octet<T, D>(a, w, b, g, exmask, row0, row1, s_hist);
         return;
     }
     using R = RowT<T, D>;
@@ -580,20 +672,26 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
     const int NG = a.B * a.Hkv;
     const int64_t len = a.len;
     uint32_t *s_hist = (uint32_t *)lds;
+    // The groups' rows are laid end to end, each group padded to a multiple of 4
+    // rows (len4), so that every segment starts on a multiple of 4; the padding
+    // rows are skipped.
+    const int64_t len4 = (len + 3) & ~(int64_t)3;
     auto do_span = [&](int n_ex, auto group_of) {
-        const int64_t total = (int64_t)n_ex * len;
+        const int64_t total = (int64_t)n_ex * len4;
         int64_t span = (total + geo.scan_blocks - 1) / geo.scan_blocks;
         span = (span + 2 * kScanRowsPerIter - 1) / (2 * kScanRowsPerIter) * (2 * kScanRowsPerIter);
         int64_t pos = (int64_t)sbk * span;
         const int64_t end = pos + span < total ? pos + span : total;
         while (pos < end) {
-            const int e = (int)(pos / len);
-            const int64_t r0 = pos - (int64_t)e * len;
-            const int64_t r1 = (r0 + (end - pos) < len) ? r0 + (end - pos) : len;
-            int gi;
-            uint32_t m;
-            group_of(e, gi, m);
-            scan_segment<T, D, G>(a, w, gi / a.Hkv, gi % a.Hkv, m, r0, r1, s_hist);
+            const int e = (int)(pos / len4);
+            const int64_t r0 = pos - (int64_t)e * len4;
+            const int64_t r1 = (r0 + (end - pos) < len4) ? r0 + (end - pos) : len4;
+            if (r0 < len) {
+                int gi;
+                uint32_t m;
+                group_of(e, gi, m);
+                scan_segment<T, D, G>(a, w, gi / a.Hkv, gi % a.Hkv, m, r0, r1 < len ? r1 : len, s_hist);
+            }
             pos += r1 - r0;
         }
     };
@@ -660,13 +758,13 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
             n_ex += (int)tot;
         }
         if (n_ex == 0) return;
-        const int64_t total = (int64_t)n_ex * len;
+        const int64_t total = (int64_t)n_ex * len4;   // the same layout as do_span
         int64_t span = (total + geo.scan_blocks - 1) / geo.scan_blocks;
         span = (span + 2 * kScanRowsPerIter - 1) / (2 * kScanRowsPerIter) * (2 * kScanRowsPerIter);
         const int64_t pos0 = (int64_t)sbk * span;
         if (pos0 >= total) return;
         const int64_t end0 = pos0 + span < total ? pos0 + span : total;
-        const int e_lo = (int)(pos0 / len), e_hi = (int)((end0 - 1) / len);
+        const int e_lo = (int)(pos0 / len4), e_hi = (int)((end0 - 1) / len4);
         // Pass 2: keep the exact groups of ranks e_lo .. e_hi.
         if (NG <= NT && m0 != 0u && e0 >= e_lo && e0 <= e_hi && e0 - e_lo < kLocalGroups)
             s_local[e0 - e_lo] = (uint32_t)tid * 256u + m0;
@@ -1496,8 +1594,6 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
 // positions at once, each against its causal prefix
 // ---------------------------------------------------------------------------
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // k_pf_score: the scores of Eq. 4 for U positions x G heads of a KV group (the
 // group's "virtual queries", vq = u * G + j) as a matrix product on the matrix
