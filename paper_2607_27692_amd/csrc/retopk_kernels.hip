@@ -498,11 +498,12 @@ __device__ void scan_segment_octet(const StepArgs &a, const Ws &w, int b, int g,
 // iteration from row0 rounded down to a multiple of 4, so that a lane's four
 // scores are one aligned 16-byte store (rows before row0 are scored, neither
 // stored nor counted); the next rows' loads are issued before the stores.
-template <int D>
+template <int D, int G>
 __device__ void scan_segment_mfma(const StepArgs &a, const Ws &w, int b, int g, uint32_t exmask,
                                   int64_t row0, int64_t row1, uint32_t *s_hist)
 {
-    constexpr int G = 8, KS = D / 32, TW = 2;
+    constexpr int KS = D / 32, TW = 2;
+    static_assert(G <= 16, "one MFMA column per head");
     constexpr int ROWS = (kScoreThreads / 64) * TW * 16;
     static_assert(D % 32 == 0 && ROWS == 2 * kScanRowsPerIter, "tile geometry");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 15, kq = lane >> 4;
@@ -581,11 +582,11 @@ template <typename T, int D, int G>
 __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint32_t exmask,
                              int64_t row0, int64_t row1, uint32_t *s_hist)
 {
-    if constexpr (G == 8) {
-        if constexpr (sizeof(T) == 2)
-            scan_segment_mfma<D>(a, w, b, g, exmask, row0, row1, s_hist);
-        else
-            scan_segment_octet<T, D>(a, w, b, g, exmask, row0, row1, s_hist);
+    if constexpr (sizeof(T) == 2 && G == 8) {
+        scan_segment_mfma<D, G>(a, w, b, g, exmask, row0, row1, s_hist);
+        return;
+    } else if constexpr (G == 8) {
+        scan_segment_octet<T, D>(a, w, b, g, exmask, row0, row1, s_hist);
         return;
     }
     using R = RowT<T, D>;
