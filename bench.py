@@ -687,9 +687,9 @@ def ablation(args):
 
 # ---- latency against context length -------------------------------------------
 def contexts(args):
-    """The headline layer (32 query / 8 KV heads, d = 128, bf16, K = 512, C = 512,
-    R = 8, W = 256, tau = 0.8, T_r = 64; one key cluster per K keys) at each prompt
-    length: mean us per step of
+    """The --workload layer (by default the headline one: 32 query / 8 KV heads,
+    d = 128, bf16, K = 512, C = 512, R = 8, W = 256, tau = 0.8, T_r = 64), with one
+    key cluster per K keys, at each prompt length: mean us per step of
     ReTopK, Exact Top-K and full attention under the cold-cache protocol, the
     fallback rate and the KV-group scans per step.  The reuse path's work does not
     depend on the context length; the exact path's grows with it (Sec. 4.3)."""
@@ -698,7 +698,7 @@ def contexts(args):
     from paper_2607_27692_amd import retopk as R
     from paper_2607_27692_amd.inputs import WORKLOADS, make_inputs
 
-    base = WORKLOADS["128k"]
+    base = WORKLOADS[args.workload]
     steps = max(1, min(args.steps, 64))
     torch.cuda.set_device(0)
     flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
@@ -762,7 +762,8 @@ def contexts(args):
         del q_tail, q_dec, k, v
         torch.cuda.empty_cache()
     print(json.dumps({"contexts": rows, "steps": steps, "data": "synthetic", "dtype": "bf16",
-                      "config": {"batch": base.batch, "q_heads": base.n_q_heads,
+                      "config": {"workload": base.name, "batch": base.batch,
+                                 "q_heads": base.n_q_heads,
                                  "kv_heads": base.n_kv_heads, "head_dim": base.head_dim,
                                  "k": base.k, "cache_cap": base.cache_cap, "r": base.r,
                                  "window": base.window, "tau": base.tau,
