@@ -24,8 +24,9 @@ def _dev_inputs(inp):
                 v=to_dev(inp.v_raw))
 
 
-def _compare_step(t, w, p, inp, gpu, orc_res, pre_state, heads, tally, q_host):
-    """gpu: dict of numpy arrays read back after the GPU step; orc_res: (out, sel, info)."""
+def _compare_step(t, w, p, kv, gpu, orc_res, pre_state, heads, tally, q_host):
+    """kv: the (K, V) arrays widened to fp32 once; gpu: dict of numpy arrays read back
+    after the GPU step; orc_res: (out, sel, info)."""
     o_out, o_sel, info = orc_res
     L = w.step_len(t)
     G = w.group
@@ -33,7 +34,7 @@ def _compare_step(t, w, p, inp, gpu, orc_res, pre_state, heads, tally, q_host):
         b, h = divmod(bh, w.n_q_heads)
         where = f"step {t} b={b} h={h}"
         q = q_host[b, h]
-        kr, vr = inp.k[b, h // G], inp.v[b, h // G]
+        kr, vr = kv[0][b, h // G], kv[1][b, h // G]
         opath, gpath = int(info.path[bh]), int(gpu["path"][bh])
         if opath != gpath:
             assert {opath, gpath} == {O.REUSE, O.FALLBACK}, f"{where}: path {gpath} vs {opath}"
@@ -85,9 +86,10 @@ def _lockstep(w, inp, p, heads, n_steps, state0=None):
     torch = torch_cuda()
     mask = np.zeros(p.heads, np.uint8)
     mask[heads] = 1
+    kf, vf = inp.k, inp.v          # widened to fp32 once
     orc = O.Oracle(p)
     if state0 is None:
-        orc.prefill_init(inp.q_tail, inp.k, inp.v, w.prompt_len, head_mask=mask)
+        orc.prefill_init(inp.q_tail, kf, vf, w.prompt_len, head_mask=mask)
     else:
         orc.set_state(*state0)
     dev = _dev_inputs(inp)
@@ -102,12 +104,14 @@ def _lockstep(w, inp, p, heads, n_steps, state0=None):
         h.set_state(pre["qbar"], pre["supp"], pre["cnt"], pre["n_inserted"], pre["t_dec"])
         L = w.step_len(t)
         h.decode_step(dev["q_dec"][t], dev["k"], dev["v"], L, out, sel, dbg)
-        res = orc.decode_step(inp.q_dec[t], inp.k, inp.v, L, head_mask=mask)
+        res = orc.decode_step(inp.q_dec[t], kf, vf, L, head_mask=mask)
         torch.cuda.synchronize()
         gpu = {k_: v_.cpu().numpy() for k_, v_ in dbg.items()}
         gpu["out"], gpu["sel"] = out.cpu().numpy(), sel.cpu().numpy()
         gpu["state"] = h.get_state()
-        _compare_step(t, w, p, inp, gpu, res, pre, heads, tally, inp.q_dec[t])
+        _compare_step(t, w, p, (kf, vf), gpu, res, pre, heads, tally, inp.q_dec[t])
+        if len(heads) > 256:
+            print(f"  step {t} compared ({len(heads)} heads)", flush=True)
         paths.append(res[2].path[heads].copy())
     h.close()
     return tally, np.array(paths)
@@ -169,6 +173,24 @@ def test_decode_lockstep_shapes(label, change):
     print(tally, flush=True)
     assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * w.steps
     assert (paths == O.REUSE).sum() > 0
+
+
+@pytest.mark.parametrize("batch", [18, 130, 512])
+def test_decode_lockstep_many_groups(batch):
+    """More KV groups than one wave (18 x 4 = 72) or one block (130 x 4 = 520) ranks
+    at once when the scan blocks look for the groups with a fallback head, up to the
+    largest head count the library takes (512 x 4 = 2048 heads): all heads, all
+    steps, in lock-step."""
+    w = WORKLOADS["16k"].with_(batch=batch, n_q_heads=4, n_kv_heads=4, prompt_len=1500 if batch < 512 else 600,
+                               steps=8, k=32, cache_cap=16, r=2, window=16, refresh=5, n_centers=8)
+    print(f"decode lock-step {batch} sequences x 4 KV groups", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w)
+    heads = list(range(w.batch * w.n_q_heads))
+    tally, paths = _lockstep(w, inp, p, heads, w.steps)
+    print(tally, flush=True)
+    assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * w.steps
+    assert (paths == O.REUSE).sum() > 0 and (paths == O.FALLBACK).sum() > 0
 
 
 def test_decode_lockstep_16k_two_groups():
