@@ -146,6 +146,11 @@ SHAPES = [
     # the largest K
     ("bf16_k2048", dict(n_q_heads=2, n_kv_heads=1, prompt_len=9000, steps=16, k=2048,
                         cache_cap=16, r=2, window=128, refresh=8, n_centers=8)),
+    # 9 000 to 12 400 candidates per reuse head (disjoint supports: frequent jumps
+    # between 20 clusters, no fallback), more than the final stage stages in LDS
+    ("bf16_cand_12k", dict(n_q_heads=2, n_kv_heads=1, prompt_len=40000, steps=12, k=2048,
+                           cache_cap=16, r=8, window=256, refresh=6, n_centers=20,
+                           p_jump=0.6, tau=-1.0)),
     # group sizes that are not powers of two: 7 (the 28 / 4 layout of the paper's
     # Qwen2.5-7B), 3 over two sequences, 5 in fp32
     ("bf16_d128_g7", dict(n_q_heads=14, n_kv_heads=2, prompt_len=5000, steps=40, k=128,

@@ -48,6 +48,9 @@ CASES = [
     ("bf16", 128, 1, 8, 2, 12000, 512, "ties"),
     ("bf16", 128, 1, 4, 1, 5000, 256, "negative"),
     ("f32", 64, 1, 1, 1, 3000, 40, "equal"),        # all scores equal: lowest indices win
+    # more survivors than the final stage stages in LDS (read from the regions)
+    ("f32", 64, 1, 1, 1, 20000, 40, "equal"),
+    ("bf16", 128, 1, 4, 1, 30000, 512, "ties"),     # about 10 000 keys tie at the top
     # group sizes that are not powers of two (padded groups)
     ("bf16", 128, 1, 28, 4, 8200, 512, "randn"),   # 7 query heads per KV head
     ("bf16", 64, 2, 6, 2, 5000, 96, "randn"),      # 3
