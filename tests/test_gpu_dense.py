@@ -28,6 +28,9 @@ CASES = [
     ("bf16", 128, 1, 28, 4, 9000),
     ("bf16", 64, 2, 6, 2, 4097),
     ("f32", 128, 1, 10, 2, 3000),
+    # the 8-head build at d = 64, bf16 and fp32
+    ("bf16", 64, 1, 8, 1, 3000),
+    ("f32", 64, 1, 16, 2, 2500),
 ]
 
 

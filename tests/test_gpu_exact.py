@@ -48,6 +48,8 @@ CASES = [
     ("bf16", 128, 1, 8, 2, 12000, 512, "ties"),
     ("bf16", 128, 1, 4, 1, 5000, 256, "negative"),
     ("f32", 64, 1, 1, 1, 3000, 40, "equal"),        # all scores equal: lowest indices win
+    # 2.2M keys: 538 filter regions, more than one per thread of the final stage
+    ("f32", 64, 1, 1, 1, 2_200_000, 512, "randn"),
     # more survivors than the final stage stages in LDS (read from the regions)
     ("f32", 64, 1, 1, 1, 20000, 40, "equal"),
     ("bf16", 128, 1, 4, 1, 30000, 512, "ties"),     # about 10 000 keys tie at the top
