@@ -72,6 +72,8 @@ def _compare_step(t, w, p, kv, gpu, orc_res, pre_state, heads, tally, q_host):
         check_output(gpu["out"][b, h], q, kr, vr, gsup, o_out[b, h], exact_set, w.dtype, where,
                      tally)
         # inserted cache entry
+        if w.cache_cap == 0:
+            continue
         slot = pre_state["n_inserted"] % w.cache_cap
         gq = gpu["state"]["qbar"][bh, slot]
         oq = O.normalize(q)
@@ -178,6 +180,27 @@ def test_decode_lockstep_shapes(label, change):
     print(tally, flush=True)
     assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * w.steps
     assert (paths == O.REUSE).sum() > 0
+
+
+@pytest.mark.parametrize("cap", [16, 0])
+def test_decode_lockstep_from_empty_cache(cap):
+    """From an empty cache the first step takes the cold exact path and inserts the
+    first entry, after which Eq. 13 decides (C = 16); with C = 0 every step is cold.
+    fp32 single head."""
+    w = WORKLOADS["tiny"].with_(cache_cap=cap)
+    print(f"decode lock-step from an empty cache, C = {cap}", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w)
+    BH = w.batch * w.n_q_heads
+    state0 = (np.zeros((BH, cap, w.head_dim), np.float32), np.full((BH, cap, w.k), -1, np.int32),
+              np.zeros((BH, cap), np.int32), 0, 0)
+    tally, paths = _lockstep(w, inp, p, [0], w.steps, state0=state0)
+    print(tally, flush=True)
+    assert tally.exact + tally.near_tie == w.steps
+    n_cold = 1 if cap else w.steps
+    assert (paths[:n_cold] == O.COLD).all()
+    if cap:
+        assert (paths[n_cold:] != O.COLD).all() and (paths == O.REUSE).sum() > 0
 
 
 @pytest.mark.parametrize("batch", [18, 130, 512])
