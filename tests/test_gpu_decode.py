@@ -182,6 +182,24 @@ def test_decode_lockstep_shapes(label, change):
     assert (paths == O.REUSE).sum() > 0
 
 
+def test_decode_lockstep_equal_keys():
+    """Identical key rows: every candidate score of a head ties, so the rerank (Eq. 11)
+    keeps the K lowest candidate indices (the radix select on ranks decides); bf16,
+    two KV groups of 2, all heads, all steps in lock-step."""
+    import dataclasses
+    w = WORKLOADS["16k"].with_(n_q_heads=4, n_kv_heads=2, prompt_len=3000, steps=24, k=128,
+                               cache_cap=16, r=4, window=64, refresh=8, n_centers=8)
+    print("decode lock-step equal keys", flush=True)
+    inp = make_inputs(w)
+    inp = dataclasses.replace(inp, k_raw=np.broadcast_to(inp.k_raw[:, :, :1], inp.k_raw.shape).copy())
+    p = params_of(w)
+    heads = list(range(w.batch * w.n_q_heads))
+    tally, paths = _lockstep(w, inp, p, heads, w.steps)
+    print(tally, flush=True)
+    assert tally.exact == len(heads) * w.steps
+    assert (paths == O.REUSE).sum() > 0
+
+
 @pytest.mark.parametrize("cap", [16, 0])
 def test_decode_lockstep_from_empty_cache(cap):
     """From an empty cache the first step takes the cold exact path and inserts the
