@@ -296,8 +296,41 @@ def _free_run(w, inp, dev, n_steps):
         sels.append(sel.cpu().numpy())
         paths.append(dbg["path"].cpu().numpy())
     st = h.stats()
+    state1 = h.get_state()
     h.close()
-    return state0, np.array(outs), np.array(sels), np.array(paths), st
+    return state0, np.array(outs), np.array(sels), np.array(paths), st, state1
+
+
+def test_side_stream_and_optional_outputs():
+    """The same 16K trajectory (prefill + 16 steps) run on a second stream without the
+    optional support and diagnostic outputs gives bitwise the outputs, cache state and
+    counters of the run on the current stream with them."""
+    torch = torch_cuda()
+    w = WORKLOADS["16k"]
+    print("side stream, optional outputs", flush=True)
+    inp = make_inputs(w)
+    dev = _dev_inputs(inp)
+    ref = _free_run(w, inp, dev, 16)
+    p = params_of(w)
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    h = handle_of(p, w.dtype)
+    outs = []
+    with torch.cuda.stream(s):
+        out = torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+        h.prefill_init(dev["q_tail"], w.cache_cap, dev["k"], dev["v"], w.prompt_len, stream=s)
+        for t in range(16):
+            h.decode_step(dev["q_dec"][t], dev["k"], dev["v"], w.step_len(t), out, None, None,
+                          stream=s)
+            outs.append(out.clone())
+    s.synchronize()
+    st = h.stats()
+    state = h.get_state()
+    h.close()
+    assert np.array_equal(np.array([o.cpu().numpy() for o in outs]), ref[1])
+    assert st == ref[4]
+    for key in ("qbar", "supp", "cnt", "n_inserted"):
+        assert np.array_equal(state[key], ref[5][key])
 
 
 def test_prefill_and_free_running_trajectory_small():
@@ -311,7 +344,7 @@ def test_prefill_and_free_running_trajectory_small():
     orc = O.Oracle(p)
     orc.prefill_init(inp.q_tail, inp.k, inp.v, w.prompt_len)
     ost = orc.get_state()
-    gst, outs, sels, paths, stats = _free_run(w, inp, dev, w.steps)
+    gst, outs, sels, paths, stats, _ = _free_run(w, inp, dev, w.steps)
     assert gst["n_inserted"] == ost["n_inserted"] == w.cache_cap
     assert np.array_equal(gst["supp"], ost["supp"])
     assert np.array_equal(gst["cnt"], ost["cnt"])
