@@ -16,8 +16,8 @@
 //   k_final   kFinalSlices blocks per head: each selects the Top-K of the head's
 //             candidates (Eq. 11) or surviving scores (Eq. 1) by radix select on
 //             64-bit ranks, then aggregates one slice of the head dimension of
-//             Softmax-V (Eq. 12); slice 0 writes the support and inserts into the
-//             cache (Sec. 3.4).
+//             Softmax-V (Eq. 12); the writes of the support and of the cache entry
+//             (Sec. 3.4) are shared out over the slices.
 // Exact Top-K attention alone is k_score (scan only) + k_filter + k_final.
 //
 // Ranking is on the fp32 scaled score fl32(q.k) * fl32(1/sqrt d) with ties to the
@@ -1556,38 +1556,49 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
             a.out[(int64_t)bh * D + slice * DS + tid] = kn > 0 ? o / l : 0.0f;
         }
     }
-    if (slice != 0) return;
-
-    if (writes_out && a.sel != nullptr)
-        for (int t = tid; t < a.K; t += NT)
-            a.sel[(int64_t)bh * a.K + t] = t < kn ? (int32_t)(sm.sel[t] >> 32) : -1;
+    // The writes that follow are shared out over the head's blocks, each of which
+    // holds the whole selection in LDS: the support output, the cache entry's
+    // support and count, its q_bar, and the counters or the histogram reset.
+    const int nblk = writes_out ? NS : 1;
+    auto owns = [&](int job) { return job % nblk == slice; };
+    if (owns(0)) {
+        if (writes_out && a.sel != nullptr)
+            for (int t = tid; t < a.K; t += NT)
+                a.sel[(int64_t)bh * a.K + t] = t < kn ? (int32_t)(sm.sel[t] >> 32) : -1;
+        if (a.dbg_ncand && tid == 0) a.dbg_ncand[bh] = reuse ? rg.n : 0;
+        if (a.dbg_cand)
+            for (int j = tid; j < a.cand_cap; j += NT)
+                a.dbg_cand[(int64_t)bh * a.cand_cap + j] = (reuse && j < rg.n) ? (int32_t)rank_index(rg.get(j)) : -1;
+    }
     if (a.do_insert) {
         // Sec. 3.4: insert (q_bar, support) after either path.
         const int64_t e = (int64_t)bh * a.M + (kMulti ? (a.insert_slot + u) % a.M : a.insert_slot);
-        if (a.mode == MODE_SELECT) {
-            for (int t = tid; t < D; t += NT) w.qbar[e * D + t] = w.qbar_cur[(int64_t)bh * D + t];
+        if (owns(1)) {
+            for (int t = tid; t < a.K; t += NT)
+                w.supp[e * a.K + t] = t < kn ? (int32_t)(sm.sel[t] >> 32) : -1;
+            if (tid == 0) w.cnt[e] = kn;
+        }
+        if (owns(2)) {
+            if (a.mode == MODE_SELECT) {
+                for (int t = tid; t < D; t += NT) w.qbar[e * D + t] = w.qbar_cur[(int64_t)bh * D + t];
+            } else {
+                const T *q = (const T *)a.q + (int64_t)bh * a.q_head_stride + (int64_t)u * D;
+                block_qbar<T, D, NT>(q, sm.qbar, sm.red64);
+                for (int t = tid; t < D; t += NT) w.qbar[e * D + t] = sm.qbar[t];
+            }
+        }
+    }
+    if (owns(3)) {
+        if (reuse) {
+            if (tid == 0) {
+                atomicAdd(&w.stats[STAT_CAND_SUM], (unsigned long long)rg.n);
+                atomicMax(&w.stats[STAT_CAND_MAX], (unsigned long long)rg.n);
+            }
         } else {
-            const T *q = (const T *)a.q + (int64_t)bh * a.q_head_stride + (int64_t)u * D;
-            block_qbar<T, D, NT>(q, sm.qbar, sm.red64);
-            for (int t = tid; t < D; t += NT) w.qbar[e * D + t] = sm.qbar[t];
+            // leave the histogram zeroed for the next launch
+            for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)vh * kHistBins + i] = 0u;
         }
-        for (int t = tid; t < a.K; t += NT)
-            w.supp[e * a.K + t] = t < kn ? (int32_t)(sm.sel[t] >> 32) : -1;
-        if (tid == 0) w.cnt[e] = kn;
     }
-    if (reuse) {
-        if (tid == 0) {
-            atomicAdd(&w.stats[STAT_CAND_SUM], (unsigned long long)rg.n);
-            atomicMax(&w.stats[STAT_CAND_MAX], (unsigned long long)rg.n);
-        }
-    } else {
-        // leave the histogram zeroed for the next launch
-        for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)vh * kHistBins + i] = 0u;
-    }
-    if (a.dbg_ncand && tid == 0) a.dbg_ncand[bh] = reuse ? rg.n : 0;
-    if (a.dbg_cand)
-        for (int j = tid; j < a.cand_cap; j += NT)
-            a.dbg_cand[(int64_t)bh * a.cand_cap + j] = (reuse && j < rg.n) ? (int32_t)rank_index(rg.get(j)) : -1;
 }
 
 // ---------------------------------------------------------------------------
