@@ -169,7 +169,8 @@ template <typename T, int D> struct RowT {
 
 // Waves per SIMD that k_score is built for: 4 (two 512-thread blocks per CU), or
 // 2 (256 registers a lane) where the group's query vectors alone would take half
-// of 128 registers (G * kNV * 4 in the quad layout, half that in the octet one).
+// of 128 registers (G * kNV * 4 in the quad layout, half that in the octet one of
+// the fp32 8-head build; the bf16 8-head build holds D / 32 MFMA operands).
 template <typename T, int D, int G>
 constexpr int kGroupWaves = (G == 8 && sizeof(T) == 2) ? 4
                             : ((G == 8 ? 2 : 4) * G * RowT<T, D>::kNV > 64 ? 2 : 4);
@@ -415,7 +416,7 @@ __host__ __device__ constexpr int score_range_lds(int n_merge)
 }
 constexpr int kLocalGroups = 512;   // exact KV groups one scan block's rows can touch
 
-// scan_segment for the 8-head build (groups of 5 to 8): a key row is split over
+// scan_segment for the fp32 8-head build (groups of 5 to 8): a key row is split over
 // the 8 lanes of an octet, lane o loading 16-byte vectors s * 8 + o, so that each
 // lane holds half the query registers of the quad layout, and after the octet
 // reduce-scatter lane o owns head o's score.  64 rows per pass of the block, 4
