@@ -66,8 +66,9 @@ def parse():
                          "layers for ReTopK, Exact Top-K and full attention (no cache flush: "
                          "rotating the layers' key and value rows defeats the caches)")
     ap.add_argument("--contexts", default="", metavar="N1,N2,...",
-                    help="instead of the one-layer protocol, time the headline layer at each "
-                         "prompt length given (ReTopK, Exact Top-K and full attention, cold "
+                    help="instead of the one-layer protocol, time the --workload layer (by "
+                         "default the headline one) at each prompt length given (ReTopK, "
+                         "Exact Top-K and full attention, cold "
                          "caches, --steps decode steps each, at most 64) and print one JSON "
                          "line with the per-length table (latency against context length)")
     ap.add_argument("--ablation", action="store_true",

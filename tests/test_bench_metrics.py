@@ -1,5 +1,6 @@
-"""The fidelity measures the benchmark reports (support recall, retained mass,
-cosine), on hand-made inputs."""
+"""Host logic of the benchmark: the fidelity measures it reports (support recall,
+retained mass, cosine) on hand-made inputs, the split of a profile into passes,
+the one-GPU guard and the traffic lookup."""
 import os
 import sys
 
@@ -69,3 +70,28 @@ def test_passes_split_the_dispatch_sequence():
     a, b = by["full timed"]
     assert names[a:b] == ["dense_chunk", "dense_merge"] * steps
     assert by["prefill"][0] == by["prefill"][1]          # no steps in the prefill pass
+
+
+def test_more_than_one_gpu_is_refused():
+    """bench.py --gpus N with N > 1 exits with a message before touching a GPU."""
+    import subprocess
+    r = subprocess.run([sys.executable, os.path.join(os.path.dirname(bench.__file__), "bench.py"),
+                        "--gpus", "2"], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "exactly one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_traffic_is_reported_only_for_the_profiled_source(monkeypatch):
+    """The measured traffic of a kernel comes from its counter summary only while the
+    kernel source still has the digest recorded with it."""
+    path = os.path.join(bench.ROOT, "profiles", "traffic_retopk_score_128k.txt")
+    with open(path) as f:
+        fields = dict(line.split(":", 1) for line in f if ":" in line)
+    digest = fields["kernel_source_sha256"].strip()
+    expected = int(float(fields["traffic_bytes_per_launch"]))
+    monkeypatch.setattr(bench, "kernel_source_digest", lambda: digest)
+    assert bench.traffic_per_launch("retopk_score", "128k") == expected
+    monkeypatch.setattr(bench, "kernel_source_digest", lambda: "0" * 64)
+    assert bench.traffic_per_launch("retopk_score", "128k") is None
+    assert bench.traffic_per_launch("no_such_kernel", "128k") is None
