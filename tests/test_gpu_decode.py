@@ -132,6 +132,20 @@ def test_decode_lockstep_small():
     assert tally.exact >= w.steps - 2
 
 
+def test_decode_lockstep_long_run():
+    """512 steps of the fp32 single-head workload with a 32-entry cache: the ring
+    buffer wraps 17 times and 31 refreshes occur, every step in lock-step."""
+    w = WORKLOADS["tiny"].with_(steps=512, cache_cap=32)
+    print(f"decode lock-step {w.name}, {w.steps} steps", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w)
+    tally, paths = _lockstep(w, inp, p, [0], w.steps)
+    print(tally, flush=True)
+    assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == w.steps
+    assert (paths == O.REFRESH).sum() == (w.steps - 1) // w.refresh
+    assert (paths == O.REUSE).sum() > w.steps // 2
+
+
 SHAPES = [
     # label, workload changes: other dtypes, head sizes and group sizes than the
     # headline layer, every head checked on every step
