@@ -416,6 +416,20 @@ __host__ __device__ constexpr int score_range_lds(int n_merge)
 }
 constexpr int kLocalGroups = 512;   // exact KV groups one scan block's rows can touch
 
+// Adds a scan segment's per-head LDS histograms (G rows of kHistBins counts) to
+// the global histograms of the group's exact heads (bits of exmask).
+template <int G>
+__device__ void flush_hist(const Ws &w, int bh0, uint32_t exmask, const uint32_t *s_hist)
+{
+    for (int i = threadIdx.x; i < G * kHistBins; i += kScoreThreads) {
+        const int j = i / kHistBins;
+        if ((exmask >> j) & 1u) {
+            const uint32_t c = s_hist[i];
+            if (c) atomicAdd(&w.hist[(int64_t)(bh0 + j) * kHistBins + (i % kHistBins)], c);
+        }
+    }
+}
+
 // scan_segment for the fp32 8-head build (groups of 5 to 8): a key row is split over
 // the 8 lanes of an octet, lane o loading 16-byte vectors s * 8 + o, so that each
 // lane holds half the query registers of the quad layout, and after the octet
@@ -480,13 +494,7 @@ __device__ void scan_segment_octet(const StepArgs &a, const Ws &w, int b, int g,
         if (base < row1) load(base);
     }
     __syncthreads();
-    for (int i = tid; i < G * kHistBins; i += kScoreThreads) {
-        const int j = i / kHistBins;
-        if ((exmask >> j) & 1u) {
-            const uint32_t c = s_hist[i];
-            if (c) atomicAdd(&w.hist[(int64_t)(bh0 + j) * kHistBins + (i % kHistBins)], c);
-        }
-    }
+    flush_hist<G>(w, bh0, exmask, s_hist);
 }
 
 // scan_segment for the bf16 8-head build on the matrix cores: with 8 query
@@ -567,13 +575,7 @@ __device__ void scan_segment_mfma(const StepArgs &a, const Ws &w, int b, int g, 
         }
     }
     __syncthreads();
-    for (int i = tid; i < G * kHistBins; i += kScoreThreads) {
-        const int j = i / kHistBins;
-        if ((exmask >> j) & 1u) {
-            const uint32_t c = s_hist[i];
-            if (c) atomicAdd(&w.hist[(int64_t)(bh0 + j) * kHistBins + (i % kHistBins)], c);
-        }
-    }
+    flush_hist<G>(w, bh0, exmask, s_hist);
 }
 
 // One contiguous segment [row0, row1) of the rows of KV group (b, g): scores of
@@ -652,13 +654,7 @@ __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint3
         if (base < row1) load(base);
     }
     __syncthreads();
-    for (int i = tid; i < G * kHistBins; i += kScoreThreads) {
-        const int j = i / kHistBins;
-        if ((exmask >> j) & 1u) {
-            const uint32_t c = s_hist[i];
-            if (c) atomicAdd(&w.hist[(int64_t)(bh0 + j) * kHistBins + (i % kHistBins)], c);
-        }
-    }
+    flush_hist<G>(w, bh0, exmask, s_hist);
 }
 
 // Scan block sbk: scores its share of the concatenated rows of the KV groups that
