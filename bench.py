@@ -905,8 +905,6 @@ def layers(args):
 # ---- profiler summaries -------------------------------------------------------
 SYMBOLS = {  # kernel symbol prefix -> name used by the library's own profiling
     "void retopk::k_sim<": "retopk_sim",
-    "void retopk::k_score<unsigned short, 128, 4, true>": "retopk_score",
-    "void retopk::k_score<unsigned short, 128, 4, false>": "retopk_scan",
     "retopk::k_filter(": "retopk_filter",
     "void retopk::k_final<": "retopk_final",
     "void retopk::k_dense<": "dense_chunk",
@@ -916,6 +914,9 @@ SYMBOLS = {  # kernel symbol prefix -> name used by the library's own profiling
 
 
 def _lib_name(symbol: str):
+    if symbol.startswith("void retopk::k_score<"):
+        # every build of k_score: <dtype, d, heads per group, selects>
+        return "retopk_score" if symbol.split(">(", 1)[0].endswith("true") else "retopk_scan"
     for prefix, name in SYMBOLS.items():
         if symbol.startswith(prefix):
             return name
@@ -991,10 +992,11 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
     passes, prefill = _passes(names, w, steps, args.warmup)
     dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3  # noqa: E731
 
+    wflag = "" if w.name == "128k" else f" --workload {w.name}"
     lines = [f"# Kernel durations, {w.name} workload, rocprofv3 kernel trace",
              "command: cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats -f csv "
-             "-d <out>/kt -o kt -- python3 -u <repo>/bench.py --no-cpu-baseline",
-             "summary: python bench.py --summarize <out>/kt <out>/pmc_fetch <out>/pmc_write",
+             f"-d <out>/kt -o kt -- python3 -u <repo>/bench.py --no-cpu-baseline{wflag}",
+             f"summary: python bench.py --summarize <out>/kt <out>/pmc_fetch <out>/pmc_write{wflag}",
              "",
              "## rocprofv3 --stats (every dispatch of the run: prefills, warm-up and all passes)",
              f"{'kernel':60s} {'library name':14s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'share':>7s}"]
@@ -1053,9 +1055,9 @@ def summarize(args, trace_dir, fetch_dir, write_dir):
         out = [f"# HBM traffic per launch of {kernel}, {w.name} workload, rocprofv3 counters",
                "command_fetch: cd /tmp && export TMPDIR=/tmp && timeout -s KILL 300 rocprofv3 "
                "--pmc FETCH_SIZE -f csv -d <out>/pmc_fetch -o pmc -- python3 -u <repo>/bench.py "
-               "--no-cpu-baseline --copy-calibration",
+               f"--no-cpu-baseline --copy-calibration{wflag}",
                "command_write: the same with --pmc WRITE_SIZE -d <out>/pmc_write",
-               "summary: python bench.py --summarize <out>/kt <out>/pmc_fetch <out>/pmc_write",
+               f"summary: python bench.py --summarize <out>/kt <out>/pmc_fetch <out>/pmc_write{wflag}",
                f"copy_bytes: {COPY_BYTES}",
                f"copy_fetch_kib: {sum(f_big) / len(f_big):.1f}",
                f"copy_write_kib: {sum(w_big) / len(w_big):.1f}",
