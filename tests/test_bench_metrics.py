@@ -95,3 +95,16 @@ def test_traffic_is_reported_only_for_the_profiled_source(monkeypatch):
     monkeypatch.setattr(bench, "kernel_source_digest", lambda: "0" * 64)
     assert bench.traffic_per_launch("retopk_score", "128k") is None
     assert bench.traffic_per_launch("no_such_kernel", "128k") is None
+
+
+def test_trace_symbols_name_every_score_build():
+    # The decode step's scoring launch and the scan-only launch are two builds of
+    # one kernel template, for every dtype, head dim and group size.
+    for dt in ("unsigned short", "float"):
+        for d in (64, 128):
+            for g in (1, 2, 4, 8):
+                sym = f"void retopk::k_score<{dt}, {d}, {g}, %s>(retopk::StepArgs, retopk::Ws)"
+                assert bench._lib_name(sym % "true") == "retopk_score"
+                assert bench._lib_name(sym % "false") == "retopk_scan"
+    assert bench._lib_name("void retopk::k_final<unsigned short, 128, true>(a)") == "retopk_final"
+    assert bench._lib_name("void at::native::reduce_kernel<512, 1>(x)") is None
