@@ -69,7 +69,9 @@ typedef struct {
     int32_t n_q_heads;   /* Hq >= 1                                              */
     int32_t n_kv_heads;  /* Hkv >= 1, Hq % Hkv == 0, 1 <= Hq / Hkv <= 8           */
     int32_t head_dim;    /* d in {64, 128}                                       */
-    int64_t max_len;     /* rows allocated per (b, KV head) in k and v, < 2^31   */
+    int64_t max_len;     /* rows allocated per (b, KV head) in k and v, 1 ..     */
+                         /* 2^24 (RETOPK_ERR_ARG from 2^31, else                */
+                         /* RETOPK_ERR_UNSUPPORTED above 2^24)                  */
     int32_t k;           /* K: support size, 1 <= K <= 2048                      */
     int32_t cache_cap;   /* C (paper), M: cache entries per query head, 0..4096  */
     int32_t r;           /* R (paper): retrieved entries per step, 1..32         */

@@ -57,7 +57,8 @@ def _cfg(**kw):
     (dict(tau=float("nan")), -1), (dict(tau=float("inf")), -1), (dict(dtype=7), -1),
     (dict(retrieval=2), -1), (dict(retrieval=-1), -1),
     (dict(head_dim=96), -2), (dict(n_q_heads=32, n_kv_heads=2), -2), (dict(k=4096), -2),
-    (dict(r=64), -2), (dict(cache_cap=8192), -2),
+    (dict(r=64), -2), (dict(cache_cap=8192), -2), (dict(max_len=(1 << 24) + 1), -2),
+    (dict(batch=65), -2),
 ])
 def test_create_rejects_bad_config(lib, bad, code):
     h = C.c_void_p()
