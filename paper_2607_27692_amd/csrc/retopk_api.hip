@@ -45,6 +45,8 @@ struct retopk_handle_s {
     int64_t last_len = 0;
     bool broken = false;
     hipStream_t last_stream = nullptr;
+    bool has_last = false;             // a call has queued work on last_stream
+    hipEvent_t order_ev = nullptr;     // orders a call on a new stream after the last
     // host-side counters (paths decided on the host)
     uint64_t steps = 0, head_steps = 0, refresh = 0, cold = 0, host_scans = 0;
     // profiling
@@ -296,6 +298,25 @@ retopk_status prefill_batched(retopk_handle h, const char *q_tail, int32_t n, in
     return st;
 }
 
+// Every call of a handle shares its caches and workspaces, so a call on another
+// stream than the previous call's first waits for the work queued there.
+retopk_status order_after_last(retopk_handle h, hipStream_t s)
+{
+    if (!h->has_last || s == h->last_stream) return RETOPK_OK;
+    if (!h->order_ev && hipEventCreateWithFlags(&h->order_ev, hipEventDisableTiming) != hipSuccess)
+        return fail(h);
+    if (hipEventRecord(h->order_ev, h->last_stream) != hipSuccess ||
+        hipStreamWaitEvent(s, h->order_ev, 0) != hipSuccess)
+        return fail(h);
+    return RETOPK_OK;
+}
+
+void set_last(retopk_handle h, hipStream_t s)
+{
+    h->last_stream = s;
+    h->has_last = true;
+}
+
 retopk_status sync_last(retopk_handle h)
 {
     if (hipSetDevice(h->device) != hipSuccess) return RETOPK_ERR_HIP;
@@ -383,6 +404,7 @@ retopk_status retopk_destroy(retopk_handle h)
     if (!h->allocs.empty()) (void)hipDeviceSynchronize();
     for (void *p : h->allocs) (void)hipFree(p);
     for (hipEvent_t e : h->ev) (void)hipEventDestroy(e);
+    if (h->order_ev) (void)hipEventDestroy(h->order_ev);
     delete h;
     return RETOPK_OK;
 }
@@ -420,9 +442,10 @@ retopk_status retopk_decode_step(retopk_handle h, const void *q, const void *k, 
     }
     hipStream_t s = (hipStream_t)stream;
     if (hipSetDevice(h->device) != hipSuccess) return fail(h);
+    if (order_after_last(h, s) != RETOPK_OK) return RETOPK_ERR_HIP;
     retopk_status st = run_step(h, a, mode, s);
     if (st != RETOPK_OK) return st;
-    h->last_stream = s;
+    set_last(h, s);
     h->last_len = len;
     const int64_t BH = heads_of(c);
     h->steps += 1;
@@ -454,9 +477,10 @@ retopk_status exact_topk_attention(retopk_handle h, const void *q, const void *k
     a.do_insert = 0;
     hipStream_t s = (hipStream_t)stream;
     if (hipSetDevice(h->device) != hipSuccess) return fail(h);
+    if (order_after_last(h, s) != RETOPK_OK) return RETOPK_ERR_HIP;
     retopk_status st = run_step(h, a, MODE_EXACT, s);
     if (st != RETOPK_OK) return st;
-    h->last_stream = s;
+    set_last(h, s);
     return RETOPK_OK;
 }
 
@@ -472,11 +496,12 @@ retopk_status retopk_prefill_init(retopk_handle h, const void *q_tail, int32_t n
     if (c.cache_cap == 0 || n == 0) return RETOPK_OK;
     hipStream_t s = (hipStream_t)stream;
     if (hipSetDevice(h->device) != hipSuccess) return fail(h);
+    if (order_after_last(h, s) != RETOPK_OK) return RETOPK_ERR_HIP;
     // Positions whose slot a later prompt-tail query overwrites (n > C) only
     // advance the insertion count.
     const int32_t u_first = n > c.cache_cap ? n - c.cache_cap : 0;
     h->n_ins += u_first;
-    h->last_stream = s;
+    set_last(h, s);
     if (c.dtype == RETOPK_BF16 && n - u_first > 1) {
         const retopk_status st = prefill_batched(h, (const char *)q_tail, n, u_first, k, v,
                                                  prefill_len, s);
@@ -500,7 +525,7 @@ retopk_status retopk_prefill_init(retopk_handle h, const void *q_tail, int32_t n
         if (st != RETOPK_OK) return st;
         h->n_ins += 1;
     }
-    h->last_stream = s;
+    set_last(h, s);
     return RETOPK_OK;
 }
 
@@ -528,6 +553,7 @@ retopk_status full_attention(retopk_handle h, const void *q, const void *k, cons
     a.do_insert = 0;
     hipStream_t s = (hipStream_t)stream;
     if (hipSetDevice(h->device) != hipSuccess) return fail(h);
+    if (order_after_last(h, s) != RETOPK_OK) return RETOPK_ERR_HIP;
     const Geometry geo = make_geometry(h, len, MODE_EXACT);
     Ws wv = h->w;
     void *args[3] = {&a, &wv, nullptr};
@@ -537,7 +563,7 @@ retopk_status full_attention(retopk_handle h, const void *q, const void *k, cons
     if (st != RETOPK_OK) return st;
     describe_kernel(KERNEL_DENSE_MERGE, h->cfg.dtype, a, geo, &d);
     if ((st = launch_desc(h, d, KID_DENSE_MERGE, args, s)) != RETOPK_OK) return st;
-    h->last_stream = s;
+    set_last(h, s);
     return RETOPK_OK;
 }
 

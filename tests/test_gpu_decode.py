@@ -347,6 +347,43 @@ def test_side_stream_and_optional_outputs():
         assert np.array_equal(state[key], ref[5][key])
 
 
+def test_calls_on_alternating_streams_are_ordered():
+    """Prefill and 16 steps alternate between two streams with no synchronisation by the
+    caller, each step queued behind a 256 MiB read on its own stream: every call waits
+    for the previous call's work, so the outputs, cache state and counters equal bitwise
+    those of the single-stream run."""
+    torch = torch_cuda()
+    from paper_2607_27692_amd import retopk as R
+    w = WORKLOADS["16k"]
+    print("alternating streams", flush=True)
+    inp = make_inputs(w)
+    dev = _dev_inputs(inp)
+    ref = _free_run(w, inp, dev, 16)
+    p = params_of(w)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    big = torch.zeros(1 << 28, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    outs = [torch.empty((w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+            for _ in range(16)]
+    h = handle_of(p, w.dtype)
+    torch.cuda.synchronize()
+    h.prefill_init(dev["q_tail"], w.cache_cap, dev["k"], dev["v"], w.prompt_len,
+                   stream=streams[1])
+    for t in range(16):
+        s = streams[t % 2]
+        R.retopk_stream_read(big, big.numel(), sink, stream=s)   # holds this stream back
+        h.decode_step(dev["q_dec"][t], dev["k"], dev["v"], w.step_len(t), outs[t], None, None,
+                      stream=s)
+    torch.cuda.synchronize()
+    st = h.stats()
+    state = h.get_state()
+    h.close()
+    assert np.array_equal(np.array([o.cpu().numpy() for o in outs]), ref[1])
+    assert st == ref[4]
+    for key in ("qbar", "supp", "cnt", "n_inserted"):
+        assert np.array_equal(state[key], ref[5][key])
+
+
 def test_prefill_and_free_running_trajectory_small():
     """GPU prefill initialisation equals the oracle's (Sec. 3.3), and the GPU's own
     64-step trajectory follows the oracle's while no near-tie intervenes."""
