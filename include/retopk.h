@@ -24,9 +24,12 @@
  *
  * Streams: the step calls are asynchronous on the HIP stream passed in
  * (a hipStream_t, NULL = the null stream); path decisions stay on the device.
+ * A call on another stream than the handle's previous call first makes that
+ * stream wait (on the device, through an event) for the work the previous call
+ * queued, since all calls of a handle share its caches and workspaces.
  * retopk_stats, retopk_get_state, retopk_set_state and retopk_profile_read
- * synchronise the stream of the last step call.  A handle is not thread-safe
- * and its step calls must not overlap.
+ * synchronise the stream of the last step call.  A handle is not thread-safe:
+ * calls on one handle must not overlap on the host.
  *
  * Errors: arguments are checked on the host before any device work; a failing
  * check returns RETOPK_ERR_ARG (or RETOPK_ERR_UNSUPPORTED for a shape the
@@ -135,7 +138,10 @@ retopk_status retopk_prefill_init(retopk_handle h, const void *q_tail, int32_t n
  * t_dec = number of earlier decode steps (the first step is t_dec = 0).  Writes
  * out (float32) and, when non-NULL, sel and the dbg arrays; inserts (q_bar,
  * support) into every head's cache.  len must satisfy 1 <= len <= max_len and
- * must not decrease between calls (RETOPK_ERR_STATE otherwise). */
+ * must not decrease between calls (RETOPK_ERR_STATE otherwise).  q, k and v must
+ * be finite: a non-finite value leaves the outputs of the heads it reaches
+ * unspecified (no memory outside the handle's buffers and the arguments is
+ * touched). */
 retopk_status retopk_decode_step(retopk_handle h, const void *q, const void *k, const void *v,
                                  int64_t len, float *out, int32_t *sel,
                                  const retopk_debug *dbg, void *stream);

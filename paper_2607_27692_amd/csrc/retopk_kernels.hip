@@ -814,6 +814,13 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     int32_t *c_rank = (int32_t *)(lds + 20 * kCands);
     const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
 
+    // Retrieved positions no list entry fills stay empty (possible only when the
+    // similarities are not ordered, e.g. NaN): they are skipped, never read.
+    if (tid < kMaxR) {
+        s_ret[tid] = -1;
+        s_retcnt[tid] = 0;
+        s_retrho[tid] = -INFINITY;
+    }
     // Independent loads first: the k_sim blocks' Top-R lists (each one sorted,
     // most similar first, invalid entries last) and q.
     const int per = a.R;                        // list length of a full k_sim block
@@ -827,7 +834,7 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
         const int32_t sl = w.topr[src];
         const double rr = w.topr_rho[src];
         const int32_t cn = w.topr_cnt[src];
-        const bool use = valid && sl >= 0;     // recent-R lists can be shorter
+        const bool use = valid && sl >= 0 && sl < M;   // recent-R lists can be shorter
         c_slot[c] = use ? sl : -1;
         c_rho[c] = use ? rr : -INFINITY;
         c_cnt[c] = use ? cn : 0;
@@ -950,8 +957,9 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
                 for (int u = 0; u < 8; ++u) {
                     const int r = r0 + u < nret ? r0 + u : 0;
                     const int t = t0 + tid < a.K ? t0 + tid : 0;
-                    const bool ok = r0 + u < nret && t0 + tid < s_retcnt[r];
-                    const int32_t x = w.supp[((int64_t)bh * M + s_ret[r]) * a.K + t];
+                    const int32_t sl = s_ret[r];
+                    const bool ok = r0 + u < nret && sl >= 0 && t0 + tid < s_retcnt[r];
+                    const int32_t x = w.supp[((int64_t)bh * M + (sl >= 0 ? sl : 0)) * a.K + t];
                     xv[u] = ok ? x : -1;
                 }
                 if (t0 == 0 && r0 == 0) {
