@@ -921,7 +921,7 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     const int64_t w0 = len - a.W > 0 ? len - a.W : 0;
     int n_win = 0;                                   // ranges covering [w0, len)
     if (a.W > 0) {
-        const int64_t share = (80ll * a.W + 10ll * a.W + 3ll * a.R * a.K - 1) / (10ll * a.W + 3ll * a.R * a.K);
+        const int64_t share = (10ll * kCandRanges * a.W + 10ll * a.W + 3ll * a.R * a.K - 1) / (10ll * a.W + 3ll * a.R * a.K);
         n_win = w0 == 0 ? kCandRanges : (int)(share < 1 ? 1 : (share > kCandRanges - 1 ? kCandRanges - 1 : share));
     }
     const int n_old = kCandRanges - n_win;           // ranges covering [0, w0)
