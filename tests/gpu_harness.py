@@ -116,3 +116,29 @@ def check_output(gout, q, kr, vr, g, oout, exact_set: bool, dtype: str, where: s
     e = rel_err(gout, ref)
     tally.max_out_err = max(tally.max_out_err, e)
     assert e <= OUT_TOL[dtype], f"{where}: output error {e:.3g} > {OUT_TOL[dtype]}"
+
+
+def divergence_is_near_tie(info, bh: int, q, krows, length: int, k: int, tau: float,
+                           r: int, pre_qbar, n_valid: int) -> bool:
+    """True when the oracle's own step for head bh sits on a near-tie that lets a
+    correct GPU step differ from it: the path decision within REL_GAP of tau, the
+    R-th and (R+1)-th cosine similarities within RHO_TIE (pre_qbar: the head's
+    cached queries before the step), or the K-th and (K+1)-th candidate scores
+    within REL_GAP relative.  Then either choice is valid and the trajectories may
+    part."""
+    path = int(info.path[bh])
+    if path in (O.REUSE, O.FALLBACK) and abs(float(info.rho_max[bh]) - tau) <= REL_GAP:
+        return True
+    if path == O.REUSE and n_valid > r:
+        rho = np.sort(pre_qbar[:n_valid].astype(np.float64) @
+                      O.normalize(q).astype(np.float64))[::-1]
+        if rho[r - 1] - rho[r] <= RHO_TIE:
+            return True
+    if path == O.REUSE:
+        universe = info.cand[bh, :int(info.n_cand[bh])]
+    else:
+        universe = np.arange(length, dtype=np.int32)
+    if universe.size <= k:
+        return False
+    s = np.sort(O.scores(q, krows, universe))[::-1]
+    return float(s[k - 1] - s[k]) <= REL_GAP * max(abs(float(s[k - 1])), 1e-30)

@@ -96,3 +96,48 @@ def test_exact_parity(dtype, d, B, Hq, Hkv, L, K, kind):
         print(f"  len={length}: {tally}", flush=True)
         assert tally.near_tie <= max(2, tally.exact // 20)
     h.close()
+
+
+@pytest.mark.parametrize("step", [0, 255])
+def test_exact_parity_headline_shape(step):
+    """The launch configuration the benchmark times as its baseline: the 128K layer
+    (32 query heads on 8 KV heads, d = 128, bf16, K = 512) on its clustered synthetic
+    keys, at the first decode step's length (131 073 keys) and the last one's
+    (131 328, a ragged filter region).  KV groups 0 and 7 (8 query heads) are
+    compared with the oracle; the other 24 heads run in the same launch."""
+    torch = torch_cuda()
+    from paper_2607_27692_amd.inputs import WORKLOADS, make_inputs
+    w = WORKLOADS["128k"]
+    length = w.step_len(step)
+    print(f"exact parity headline shape, len {length}", flush=True)
+    inp = make_inputs(w)
+    p = O.Params(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.max_len, w.k, w.cache_cap,
+                 w.r, w.window, w.tau, w.refresh)
+    heads = list(range(0, w.group)) + list(range(w.n_q_heads - w.group, w.n_q_heads))
+    mask = np.zeros(p.heads, np.uint8)
+    mask[heads] = 1
+    kf, vf = inp.k, inp.v              # widened to fp32 once
+    q = inp.q_dec[step]
+    o_out, o_sel, _ = O.exact(p, q, kf, vf, length, head_mask=mask)
+    h = handle_of(p, w.dtype)
+    out = torch.empty((1, w.n_q_heads, w.head_dim), dtype=torch.float32, device="cuda")
+    sel = torch.full((1, w.n_q_heads, w.k), -7, dtype=torch.int32, device="cuda")
+    h.exact(to_dev(inp.q_dec_raw[step]), to_dev(inp.k_raw), to_dev(inp.v_raw), length, out, sel)
+    torch.cuda.synchronize()
+    g_out, g_sel = out.cpu().numpy(), sel.cpu().numpy()
+    h.close()
+    tally = Tally()
+    universe = np.arange(length, dtype=np.int32)
+    for hh in heads:
+        kr, vr = kf[0, hh // w.group, :length], vf[0, hh // w.group, :length]
+        us = O.scores(q[0, hh], kr, universe)
+        where = f"len={length} h={hh}"
+        gsup = check_selection(g_sel[0, hh], o_sel[0, hh], universe, us, where, tally)
+        exact_set = np.array_equal(gsup, o_sel[0, hh][o_sel[0, hh] >= 0])
+        check_output(g_out[0, hh], q[0, hh], kr, vr, gsup, o_out[0, hh], exact_set, w.dtype,
+                     where, tally)
+    # the heads the oracle did not compute are still complete supports
+    assert (g_sel >= 0).all() and (g_sel < length).all()
+    assert (np.diff(g_sel, axis=-1) > 0).all()
+    print(f"  {tally}", flush=True)
+    assert tally.exact + tally.near_tie == len(heads) and tally.near_tie <= 2
