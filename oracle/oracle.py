@@ -38,12 +38,14 @@ _LIB = None
 
 
 def load(path: str | None = None):
-    """Load (building first if needed) the oracle shared library."""
+    """Load (building first if needed) the oracle shared library.  The environment
+    variable RETOPK_ORACLE_LIB names another build of it (the sanitizer test)."""
     global _LIB
     if path is None and _LIB is not None:
         return _LIB
-    path = path or _build.LIB
-    if not os.path.exists(path):
+    default = path is None
+    path = path or os.environ.get("RETOPK_ORACLE_LIB") or _build.LIB
+    if not os.path.exists(path) and path == _build.LIB:
         _build.build()
     lib = C.CDLL(path)
     P = C.c_void_p
@@ -67,7 +69,7 @@ def load(path: str | None = None):
     lib.orc_normalize.restype = None
     lib.orc_attend.argtypes = [P, P, P, C.c_int32, C.c_int64, P, P]
     lib.orc_attend.restype = None
-    if path == _build.LIB:
+    if default:
         _LIB = lib
     return lib
 

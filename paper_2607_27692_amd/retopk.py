@@ -56,11 +56,13 @@ _LIB = None
 
 def load(path: str | None = None):
     """Load the built library.  Raises if it has not been built: there is no
-    fallback implementation."""
+    fallback implementation.  The environment variable RETOPK_LIB names another
+    build of it (the host-sanitizer test)."""
     global _LIB
     if _LIB is not None and path is None:
         return _LIB
-    path = path or _build.LIB
+    default = path is None
+    path = path or os.environ.get("RETOPK_LIB") or _build.LIB
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
                            "(hipcc --offload-arch=gfx950)")
@@ -86,7 +88,7 @@ def load(path: str | None = None):
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = res
-    if path == _build.LIB:
+    if default:
         _LIB = lib
     return lib
 
