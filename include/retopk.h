@@ -56,7 +56,9 @@ typedef enum {
     RETOPK_ERR_UNSUPPORTED = -2,  /* valid, but no kernel for this shape        */
     RETOPK_ERR_OOM = -3,          /* device allocation failed in retopk_create  */
     RETOPK_ERR_HIP = -4,          /* a HIP runtime call failed                  */
-    RETOPK_ERR_STATE = -5         /* call out of order (see each function)      */
+    RETOPK_ERR_STATE = -5,        /* call out of order (see each function)      */
+    RETOPK_ERR_TOO_LARGE = -6     /* the call needs more workspace than the     */
+                                  /* fixed scratch of exact_topk_attention_noalloc */
 } retopk_status;
 
 /* Path taken by one (sequence, query head) in one step (Eq. 13). */
@@ -169,6 +171,33 @@ retopk_status retopk_stream_read(const void *src, int64_t bytes, uint32_t *sink,
 retopk_status exact_topk_attention(retopk_handle h, const void *q, const void *k,
                                    const void *v, int64_t len, float *out, int32_t *sel,
                                    void *stream);
+
+/* Size of the fixed device scratch array behind exact_topk_attention_noalloc,
+ * in MiB (one copy per GPU the library runs on, held until the process ends). */
+#define RETOPK_NOALLOC_SCRATCH_MB 64
+
+/* exact_topk_attention for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  No handle: cfg describes the layer as for retopk_create (only
+ * its shape fields, K and dtype matter here) and is validated the same way; q,
+ * k, v, len, out, sel and stream are as for exact_topk_attention, and the
+ * result is the same (the same kernels run).  The workspaces come from a fixed
+ * array of RETOPK_NOALLOC_SCRATCH_MB MiB of device memory inside the library,
+ * of which one call uses, with BH = batch * n_q_heads and
+ * R = 4096 * ceil(len / 4096),
+ *   BH * (12 * R + 8192 + 4 * R / 4096 + 32) bytes (each of the five parts
+ *   rounded up to 256 bytes);
+ * a larger call returns RETOPK_ERR_TOO_LARGE before any device work (the 128K
+ * layer of 32 query heads, len 131 328, needs 52 MB).  Nothing is allocated:
+ * neither hipMalloc nor hipFree nor any allocating library routine is called
+ * (the first call on a device looks up the array's address there).  Every call
+ * on one GPU shares that GPU's array: calls that overlap on one GPU (different
+ * streams or host threads without ordering between them) race and give
+ * undefined results.  Each call clears what must start at zero with a kernel
+ * (no memset node), so it can be captured in a HIP graph. */
+retopk_status exact_topk_attention_noalloc(const retopk_config *cfg, const void *q,
+                                           const void *k, const void *v, int64_t len,
+                                           float *out, int32_t *sel, void *stream);
 
 /* Read the cumulative counters (synchronises). */
 retopk_status retopk_stats(retopk_handle h, retopk_stats_t *out);

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libretopk.so")
 SOURCES = [os.path.join(CSRC, "retopk_kernels.hip"), os.path.join(CSRC, "retopk_api.hip"),
-           os.path.join(CSRC, "retopk_stream.hip")]
+           os.path.join(CSRC, "retopk_stream.hip"), os.path.join(CSRC, "retopk_noalloc.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -57,10 +57,7 @@ struct retopk_handle_s {
     size_t ev_used = 0;
 };
 
-namespace {
-
-int64_t heads_of(const retopk_config &c) { return (int64_t)c.batch * c.n_q_heads; }
-size_t elem_size(const retopk_config &c) { return c.dtype == RETOPK_BF16 ? 2 : 4; }
+namespace retopk {
 
 retopk_status validate_config(const retopk_config *c)
 {
@@ -83,8 +80,56 @@ retopk_status validate_config(const retopk_config *c)
     return RETOPK_OK;
 }
 
-bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
-int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+StepArgs config_args(const retopk_config &c)
+{
+    StepArgs a{};
+    a.B = c.batch;
+    a.Hq = c.n_q_heads;
+    a.Hkv = c.n_kv_heads;
+    a.G = c.n_q_heads / c.n_kv_heads;
+    a.D = c.head_dim;
+    a.max_len = c.max_len;
+    a.K = c.k;
+    a.M = c.cache_cap;
+    a.R = c.r;
+    a.W = c.window;
+    a.cand_cap = c.r * c.k + c.window;
+    a.n_regions = (int)ceil_div(c.max_len, kFilterRows);
+    a.n_dense = (int)ceil_div(c.max_len, kDenseRows);
+    a.row_stride = (int64_t)a.n_regions * kFilterRows;
+    a.tau = c.tau;
+    a.retrieval = c.retrieval;
+    a.inv_sqrt_d = (float)(1.0 / std::sqrt((double)c.head_dim));
+    a.q_head_stride = c.head_dim;
+    a.U = 1;
+    return a;
+}
+
+Geometry step_geometry(const retopk_config &c, int64_t len, int mode)
+{
+    Geometry g{};
+    // Enough scan blocks to cover the whole chip when every group is scanned;
+    // fewer in MODE_SELECT, where the range blocks share the chip.
+    const int64_t rows = (int64_t)c.batch * c.n_kv_heads * len;
+    const int64_t want = ceil_div(rows, 2 * kScanRowsPerIter);
+    // In MODE_SELECT the scan shares the launch with the range blocks and covers
+    // only the groups with a fallback head: a fixed number of blocks per KV group,
+    // so that a step where most groups fall back still spreads over the chip.
+    int64_t sel_cap = (int64_t)kScanBlocksPerGroup * c.batch * c.n_kv_heads;
+    sel_cap = sel_cap < kScanBlocksSelect ? kScanBlocksSelect
+                                          : (sel_cap > kScanBlocksExact ? kScanBlocksExact : sel_cap);
+    const int cap = mode == MODE_SELECT ? (int)sel_cap : kScanBlocksExact;
+    g.scan_blocks = (int)(want < cap ? want : cap);
+    g.cand_blocks = mode == MODE_SELECT ? (int)(heads_of(c) * kCandRanges) : 0;
+    g.filter_blocks_per_head = (int)ceil_div(len, kFilterRows);
+    return g;
+}
+
+}  // namespace retopk
+
+namespace {
+
+size_t elem_size(const retopk_config &c) { return c.dtype == RETOPK_BF16 ? 2 : 4; }
 
 template <typename T>
 retopk_status alloc(retopk_handle h, T **out, size_t count)
@@ -102,51 +147,11 @@ retopk_status alloc(retopk_handle h, T **out, size_t count)
     return RETOPK_OK;
 }
 
-StepArgs base_args(const retopk_handle_s *h)
-{
-    const retopk_config &c = h->cfg;
-    StepArgs a{};
-    a.B = c.batch;
-    a.Hq = c.n_q_heads;
-    a.Hkv = c.n_kv_heads;
-    a.G = h->G;
-    a.D = c.head_dim;
-    a.max_len = c.max_len;
-    a.K = c.k;
-    a.M = c.cache_cap;
-    a.R = c.r;
-    a.W = c.window;
-    a.cand_cap = h->cand_cap;
-    a.n_regions = (int)ceil_div(c.max_len, kFilterRows);
-    a.n_dense = (int)ceil_div(c.max_len, kDenseRows);
-    a.row_stride = (int64_t)a.n_regions * kFilterRows;
-    a.tau = c.tau;
-    a.retrieval = c.retrieval;
-    a.inv_sqrt_d = h->inv_sqrt_d;
-    a.q_head_stride = c.head_dim;
-    a.U = 1;
-    return a;
-}
+StepArgs base_args(const retopk_handle_s *h) { return config_args(h->cfg); }
 
 Geometry make_geometry(const retopk_handle_s *h, int64_t len, int mode)
 {
-    const retopk_config &c = h->cfg;
-    Geometry g{};
-    // Enough scan blocks to cover the whole chip when every group is scanned;
-    // fewer in MODE_SELECT, where the range blocks share the chip.
-    const int64_t rows = (int64_t)c.batch * c.n_kv_heads * len;
-    const int64_t want = ceil_div(rows, 2 * kScanRowsPerIter);
-    // In MODE_SELECT the scan shares the launch with the range blocks and covers
-    // only the groups with a fallback head: a fixed number of blocks per KV group,
-    // so that a step where most groups fall back still spreads over the chip.
-    int64_t sel_cap = (int64_t)kScanBlocksPerGroup * c.batch * c.n_kv_heads;
-    sel_cap = sel_cap < kScanBlocksSelect ? kScanBlocksSelect
-                                          : (sel_cap > kScanBlocksExact ? kScanBlocksExact : sel_cap);
-    const int cap = mode == MODE_SELECT ? (int)sel_cap : kScanBlocksExact;
-    g.scan_blocks = (int)(want < cap ? want : cap);
-    g.cand_blocks = mode == MODE_SELECT ? (int)(heads_of(c) * kCandRanges) : 0;
-    g.filter_blocks_per_head = (int)ceil_div(len, kFilterRows);
-    return g;
+    return step_geometry(h->cfg, len, mode);
 }
 
 // Event pair for the next launch of kernel `kid` when profiling is on.
@@ -337,6 +342,7 @@ const char *retopk_status_string(retopk_status s)
     case RETOPK_ERR_OOM: return "device out of memory";
     case RETOPK_ERR_HIP: return "HIP runtime error";
     case RETOPK_ERR_STATE: return "call out of order or handle broken";
+    case RETOPK_ERR_TOO_LARGE: return "workspace larger than the fixed scratch";
     }
     return "unknown status";
 }

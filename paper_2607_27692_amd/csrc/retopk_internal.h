@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "retopk.h"
+
 namespace retopk {
 
 // Score histogram used by the full-history selection: bins are the top 11 bits
@@ -146,6 +148,17 @@ enum : int { KERNEL_SIM = 0, KERNEL_SCORE = 1, KERNEL_FILTER = 2, KERNEL_FINAL =
 constexpr int kDenseRows = 1024;
 constexpr int kDenseThreads = 512;
 constexpr int kMergeThreads = 1024;  // dense merge block: one per query head
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+inline int64_t heads_of(const retopk_config &c) { return (int64_t)c.batch * c.n_q_heads; }
+
+// Host helpers shared by the entry points (retopk_api.hip): the configuration
+// check of retopk_create, the launch arguments a configuration fixes (every
+// step-dependent field left zero), and the launch geometry of a step.
+retopk_status validate_config(const retopk_config *c);
+StepArgs config_args(const retopk_config &c);
+Geometry step_geometry(const retopk_config &c, int64_t len, int mode);
 
 // Fills *k for kernel `which` of a step in a.mode (retopk_kernels.hip).
 // dtype: 0 = f32, 1 = bf16.

@@ -16,11 +16,13 @@ RETOPK_F32, RETOPK_BF16 = 0, 1
 REUSE, FALLBACK, REFRESH, COLD = 0, 1, 2, 3
 PATH_NAMES = {REUSE: "reuse", FALLBACK: "fallback", REFRESH: "refresh", COLD: "cold"}
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported shape", -3: "device out of memory",
-          -4: "HIP runtime error", -5: "call out of order or handle broken"}
+          -4: "HIP runtime error", -5: "call out of order or handle broken",
+          -6: "workspace larger than the fixed scratch"}
 
 # Every symbol include/retopk.h declares.
 EXPORTS = ("retopk_create", "retopk_destroy", "retopk_prefill_init", "retopk_decode_step",
-           "exact_topk_attention", "full_attention", "retopk_stream_read", "retopk_stats",
+           "exact_topk_attention", "exact_topk_attention_noalloc", "full_attention",
+           "retopk_stream_read", "retopk_stats",
            "retopk_get_state",
            "retopk_set_state",
            "retopk_profile", "retopk_profile_read", "retopk_kernel_name",
@@ -74,6 +76,8 @@ def load(path: str | None = None):
         "retopk_prefill_init": ([P, P, I32, P, P, I64, P], C.c_int),
         "retopk_decode_step": ([P, P, P, P, I64, P, P, C.POINTER(retopk_debug), P], C.c_int),
         "exact_topk_attention": ([P, P, P, P, I64, P, P, P], C.c_int),
+        "exact_topk_attention_noalloc": ([C.POINTER(retopk_config), P, P, P, I64, P, P, P],
+                                         C.c_int),
         "full_attention": ([P, P, P, P, I64, P, P], C.c_int),
         "retopk_stream_read": ([P, I64, P, P], C.c_int),
         "retopk_stats": ([P, C.POINTER(retopk_stats_t)], C.c_int),
@@ -156,6 +160,14 @@ def retopk_decode_step(h, q, k, v, length, out, sel=None, dbg: dict | None = Non
 def exact_topk_attention(h, q, k, v, length, out, sel=None, stream=None) -> None:
     _check("exact_topk_attention", load().exact_topk_attention(
         h, _addr(q), _addr(k), _addr(v), length, _addr(out), _addr(sel), _stream(stream)))
+
+
+def exact_topk_attention_noalloc(cfg: retopk_config, q, k, v, length, out, sel=None,
+                                 stream=None) -> None:
+    """exact_topk_attention without a handle, on the library's fixed scratch."""
+    _check("exact_topk_attention_noalloc", load().exact_topk_attention_noalloc(
+        C.byref(cfg), _addr(q), _addr(k), _addr(v), length, _addr(out), _addr(sel),
+        _stream(stream)))
 
 
 def full_attention(h, q, k, v, length, out, stream=None) -> None:

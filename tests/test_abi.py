@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for code in (0, -1, -2, -3, -4, -5):
+    for code in (0, -1, -2, -3, -4, -5, -6):
         assert R.retopk_status_string(code) == R.STATUS[code]
     assert [R.retopk_kernel_name(i) for i in range(8)] == [
         "retopk_sim", "retopk_score", "retopk_scan", "retopk_filter", "retopk_final",
@@ -83,3 +83,38 @@ def test_null_arguments(lib):
     st = R.retopk_stats_t()
     assert lib.retopk_stats(None, C.byref(st)) == -1
     assert lib.retopk_profile(None, 1) == -1
+
+
+def test_noalloc_entry_point_checks_on_the_host(lib):
+    """exact_topk_attention_noalloc validates its configuration and arguments, and
+    refuses a call whose workspace exceeds the fixed scratch, before any device
+    work (no GPU needed)."""
+    fn = lib.exact_topk_attention_noalloc
+    ok = _cfg(max_len=131328)
+    assert fn(None, 16, 16, 16, 1, 16, None, None) == -1                  # no config
+    bad = _cfg(batch=0)
+    assert fn(C.byref(bad), 16, 16, 16, 1, 16, None, None) == -1
+    unsup = _cfg(head_dim=96)
+    assert fn(C.byref(unsup), 16, 16, 16, 1, 16, None, None) == -2
+    assert fn(C.byref(ok), None, 16, 16, 1, 16, None, None) == -1         # null q
+    assert fn(C.byref(ok), 16, 16, 16, 1, None, None, None) == -1        # null out
+    assert fn(C.byref(ok), 8, 16, 16, 1, 16, None, None) == -1           # misaligned q
+    assert fn(C.byref(ok), 16, 16, 16, 0, 16, None, None) == -1          # len 0
+    assert fn(C.byref(ok), 16, 16, 16, 131329, 16, None, None) == -1     # len > max_len
+    # 128 heads at 64K (the 4-sequence layer) need about 108 MB of workspace
+    big = _cfg(batch=4, max_len=65792)
+    assert fn(C.byref(big), 16, 16, 16, 65792, 16, None, None) == -6
+    # the same heads at 16K fit: that call would reach the device, so it is not made here
+    assert R.retopk_status_string(-6) == R.STATUS[-6]
+
+
+def test_noalloc_workspace_formula():
+    """The workspace size documented in include/retopk.h for the fixed scratch: the
+    128K layer of 32 query heads fits, the 4-sequence 64K layer does not."""
+    def need(bh, length):
+        r = 4096 * -(-length // 4096)
+        parts = [bh * r * 4, bh * r * 8, bh * 8192, bh * (r // 4096) * 4, bh * 32]
+        return sum(-(-p // 256) * 256 for p in parts)
+    limit = 64 << 20
+    assert need(32, 131328) <= limit < need(128, 65792)
+    assert abs(need(32, 131328) / 1e6 - 52.2) < 0.1
