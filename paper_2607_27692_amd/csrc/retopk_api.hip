@@ -120,7 +120,8 @@ Geometry step_geometry(const retopk_config &c, int64_t len, int mode)
                                           : (sel_cap > kScanBlocksExact ? kScanBlocksExact : sel_cap);
     const int cap = mode == MODE_SELECT ? (int)sel_cap : kScanBlocksExact;
     g.scan_blocks = (int)(want < cap ? want : cap);
-    g.cand_blocks = mode == MODE_SELECT ? (int)(heads_of(c) * kCandRanges) : 0;
+    // range blocks: whole groups of 8 heads (one head per XCD)
+    g.cand_blocks = mode == MODE_SELECT ? (int)((heads_of(c) + 7) / 8 * 8 * kCandRanges) : 0;
     g.filter_blocks_per_head = (int)ceil_div(len, kFilterRows);
     return g;
 }

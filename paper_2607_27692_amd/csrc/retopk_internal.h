@@ -18,7 +18,7 @@ constexpr int kSimThreads = 256;      // k_sim: 64 cached slots per block
 constexpr int kSimSlots = 64;
 constexpr int kScoreThreads = 512;    // k_score and k_filter blocks
 constexpr int kFinalThreads = 512;    // k_final blocks
-constexpr int kFinalSlices = 4;       // k_final blocks per head (one d-slice of V each)
+constexpr int kFinalSlices = 8;       // k_final blocks per head (one d-slice of V each)
 constexpr int kScanRowsPerIter = 128; // 8 waves x 16 rows
 constexpr int kCandRanges = 8;        // index ranges (k_score blocks) per reuse head
 constexpr int kCandList = 2048;       // candidates gathered per round in one range block
@@ -124,7 +124,7 @@ struct StepArgs {
 // Launch geometry chosen on the host.
 struct Geometry {
     int scan_blocks;           // scan blocks of k_score (they split the scanned rows)
-    int cand_blocks;           // B * Hq * kCandRanges in MODE_SELECT, else 0
+    int cand_blocks;           // ceil(B * Hq / 8) * 8 * kCandRanges in MODE_SELECT, else 0
     int filter_blocks_per_head;
     // batched prefill (k_pf_score): (KV group, key chunk) pairs, query tiles of
     // kPfCols virtual queries, key chunks of kPfKeys keys per group

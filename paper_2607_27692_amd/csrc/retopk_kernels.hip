@@ -14,11 +14,16 @@
 //   k_filter  per exact head, the scores at or above the histogram bin that holds
 //             the K-th largest, compacted in index order.
 //   k_final   kFinalSlices blocks per head: each selects the Top-K of the head's
-//             candidates (Eq. 11) or surviving scores (Eq. 1) by radix select on
-//             64-bit ranks, then aggregates one slice of the head dimension of
-//             Softmax-V (Eq. 12); the writes of the support and of the cache entry
+//             candidates (Eq. 11) or surviving scores (Eq. 1) -- entries held in
+//             registers, value-linear score bins, the threshold bin ranked exactly
+//             (a radix select on 64-bit ranks for the heads that do not fit) --
+//             then aggregates one slice of the head dimension of Softmax-V
+//             (Eq. 12); the writes of the support and of the cache entry
 //             (Sec. 3.4) are shared out over the slices.
 // Exact Top-K attention alone is k_score (scan only) + k_filter + k_final.
+// A head's similarity, range and final blocks run on one XCD (blocks are placed
+// on XCDs round-robin by block index), so that blocks sharing a head's data
+// (Top-R lists, supports, value rows) share that XCD's L2.
 //
 // Ranking is on the fp32 scaled score fl32(q.k) * fl32(1/sqrt d) with ties to the
 // lower index: every entry carries a 64-bit rank (score key << 32 | ~index), and
@@ -108,15 +113,18 @@ __device__ __forceinline__ double quad_sum(double x)
     return x;
 }
 
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v)
+// Inclusive prefix sum over the 64 lanes of a wave: Hillis-Steele inside each row
+// of 16 lanes (DPP row shifts, lanes shifted in from outside the row read 0), then
+// the row totals carried across rows with the row broadcasts of lanes 15 and 31.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
 {
-    const int l = threadIdx.x & 63;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        uint32_t t = __shfl_up(v, o);
-        if (l >= o) v += t;
-    }
-    return v;
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, false);  // row_shr:2
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, false);  // row_shr:4
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, false);  // row_shr:8
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+    return x;
 }
 
 // Block reductions.  All threads must call them; every thread gets the same
@@ -319,7 +327,11 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3;
     const int M = a.M;
     const int nsb = (M + kSimSlots - 1) / kSimSlots;
-    const int bh = blockIdx.x / nsb, sb = blockIdx.x % nsb;
+    // the nsb blocks of head bh run on XCD bh % 8 (block j is placed on XCD j % 8),
+    // with the head's range blocks and final blocks, which read what they write
+    const int xcd = (int)blockIdx.x & 7, rest = (int)blockIdx.x >> 3;
+    const int sb = rest % nsb, bh = (rest / nsb) * 8 + xcd;
+    if (bh >= a.B * a.Hq) return;
     const int n_valid = (int)(a.n_ins < (int64_t)M ? a.n_ins : (int64_t)M);
 
     // Eq. 6: 16 slots per wave, 4 lanes per cached row of D floats.  The cached
@@ -802,7 +814,11 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     __shared__ int32_t s_retcnt[kMaxR];
     __shared__ double s_retrho[kMaxR];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
-    const int bh = cb / kCandRanges, s = cb % kCandRanges;
+    // the kCandRanges blocks of head bh run on XCD bh % 8 (block j is placed on
+    // XCD j % 8), beside the head's similarity blocks and final blocks
+    const int xcd = cb & 7, rest = cb >> 3;
+    const int s = rest % kCandRanges, bh = (rest / kCandRanges) * 8 + xcd;
+    if (bh >= a.B * a.Hq) return;
     const int M = a.M;
     const int n_valid = (int)(a.n_ins < (int64_t)M ? a.n_ins : (int64_t)M);
     const int nsb = (M + kSimSlots - 1) / kSimSlots;
@@ -1275,6 +1291,489 @@ __device__ bool value_threshold(const uint64_t *ent, int n, int K, FinalSmem<D, 
     return true;
 }
 
+// ---------------------------------------------------------------------------
+// k_final fast path (decode steps and Exact Top-K): the head's entries stay in
+// registers, up to kFastEPT consecutive ones per thread (thread order is index
+// order), loaded with the region counts in one round trip when the speculation
+// holds, else in a second one; every wave derives the region offsets and the
+// threshold bin itself; the selected entries go to an index-ordered list in LDS,
+// from which dense row loads feed Softmax-V.  Heads that do not fit (more than
+// kFastRegions regions, more entries than the threads can hold, a degenerate
+// score range, or more than kTieMax entries in the threshold bin after two levels
+// of bins) take the general path below, which reloads everything.
+// ---------------------------------------------------------------------------
+
+constexpr int kFastEPT = 8;                            // consecutive entries per thread
+constexpr int kFastSlots = kFinalThreads * kFastEPT;   // entries one block holds
+constexpr int kFastBins = 512;                         // value-linear score bins
+constexpr int kFastRegions = 64;                       // regions one wave ranks
+
+
+// Reductions over a wave: DPP inside each row of 16 lanes (quad swaps, half-row
+// and row mirrors), then the four row results read as scalars.  Every lane gets
+// the result.
+__device__ __forceinline__ uint32_t row_max_u32(uint32_t x)
+{
+    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, kQuadXor1, 0xF, 0xF, true));
+    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, kQuadXor2, 0xF, 0xF, true));
+    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, kHalfMirror, 0xF, 0xF, true));
+    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x140, 0xF, 0xF, true));   // row_mirror
+    return x;
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x)
+{
+    x = row_max_u32(x);
+    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 0);
+    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 16);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 32);
+    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)x, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+__device__ __forceinline__ float wave_sum_f32(float x)
+{
+    x += dpp_f32<kQuadXor1>(x);
+    x += dpp_f32<kQuadXor2>(x);
+    x += dpp_f32<kHalfMirror>(x);
+    x += dpp_f32<0x140>(x);   // row_mirror
+    const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 0));
+    const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 16));
+    const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 32));
+    const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 48));
+    return (r0 + r1) + (r2 + r3);
+}
+
+// x from lane (i + n) mod 16 of the same row of 16 lanes (DPP row_ror:n, 1..15).
+__device__ __forceinline__ float row_ror_f32(float x, int n)
+{
+    int r;
+    switch (n) {
+    case 1: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x121, 0xF, 0xF, true); break;
+    case 2: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x122, 0xF, 0xF, true); break;
+    case 4: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x124, 0xF, 0xF, true); break;
+    default: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x128, 0xF, 0xF, true); break;
+    }
+    return __builtin_bit_cast(float, r);
+}
+
+struct FastSmem {
+    uint32_t hist[kFastBins];
+    uint64_t tie[kTieMax];
+    uint32_t wmax[kFinalThreads / 64], wmin[kFinalThreads / 64];
+    uint32_t wsel[kFinalThreads / 64];
+    uint32_t n_tie;
+};
+
+// The bin b* that holds the k-th largest of the entries counted in hist (nb bins,
+// descending from bin nb - 1), the count above it and its own count, found by one
+// wave (every wave gets the same result): lane l sums bins nb-1-BPL*l ..
+// nb-BPL-BPL*l, a wave prefix sum finds the lane, that lane walks its bins.
+template <int NB>
+__device__ __forceinline__ void wave_find_bin(const uint32_t *hist, uint32_t k, uint32_t &bstar,
+                                              uint32_t &above, uint32_t &cnt)
+{
+    constexpr int BPL = NB / 64;
+    static_assert(BPL % 4 == 0, "whole 16-byte reads");
+    const int lane = threadIdx.x & 63;
+    uint32_t c[BPL], mine = 0u;
+    const uint4 *hv = (const uint4 *)&hist[NB - BPL * (lane + 1)];
+#pragma unroll
+    for (int i = 0; i < BPL / 4; ++i) {
+        const uint4 x = hv[i];
+        c[BPL - 1 - 4 * i] = x.x;
+        c[BPL - 2 - 4 * i] = x.y;
+        c[BPL - 3 - 4 * i] = x.z;
+        c[BPL - 4 - 4 * i] = x.w;
+    }
+#pragma unroll
+    for (int i = 0; i < BPL; ++i) mine += c[i];
+    const uint32_t inc = wave_incl_scan(mine);
+    const uint64_t hit = __ballot(inc - mine < k && inc >= k);
+    const int src = __builtin_ctzll(hit);   // k <= total: exactly one lane
+    uint32_t bs = 0u, ab = 0u, cb = 0u, run = inc - mine;
+#pragma unroll
+    for (int i = 0; i < BPL; ++i) {
+        if (run < k && run + c[i] >= k) {
+            bs = (uint32_t)(NB - 1 - BPL * lane - i);
+            ab = run;
+            cb = c[i];
+        }
+        run += c[i];
+    }
+    bstar = (uint32_t)__builtin_amdgcn_readlane((int)bs, src);
+    above = (uint32_t)__builtin_amdgcn_readlane((int)ab, src);
+    cnt = (uint32_t)__builtin_amdgcn_readlane((int)cb, src);
+}
+
+// Block (bh, slice) of k_final on the fast path.  Returns false, with every thread
+// agreeing and nothing written yet, when the head must take the general path.
+template <typename T, int D>
+__device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, FastSmem &fs,
+                           uint64_t *stage, uint64_t *list, float (*part)[D / kFinalSlices + 1])
+{
+    constexpr int NT = kFinalThreads, NW = NT / 64, EPT = kFastEPT;
+    constexpr int DS = D / kFinalSlices;                  // elements of this block's slice
+    constexpr int EPV = 16 / (int)sizeof(T);
+    constexpr int LPR = DS * (int)sizeof(T) / 16;         // lanes per slice row
+    constexpr int RPW = 64 / LPR;                         // rows per wave instruction
+    static_assert(LPR >= 1 && LPR <= 16 && DS * (int)sizeof(T) == LPR * 16, "slice geometry");
+    static_assert(EPT <= 32 && EPT % 2 == 0, "entry masks");
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const bool sel_mode = a.mode == MODE_SELECT;
+    const int64_t len = a.len;
+    const int nreg_x = (int)((len + kFilterRows - 1) / kFilterRows);   // exact layout
+
+    for (int i = tid; i < kFastBins; i += NT) fs.hist[i] = 0u;
+    if (tid == 0) fs.n_tie = 0u;
+
+    // Entries in registers, thread order = index order: thread t holds entries
+    // j0 .. j0+EPT-1 of region r_me (regions in index order, entries ascending),
+    // each region taking ceil(count / EPT) consecutive threads, so the live
+    // entries sit in the first threads and the other waves skip the per-entry
+    // work.  First round trip: the path, the counts of both layouts and,
+    // speculatively, EPT entries per thread of the expected layout (the candidate
+    // ranges for a decode step that selects, the survivor regions otherwise),
+    // each region taking an equal share of the slots.  When the speculation holds,
+    // its entries are repacked through LDS; when the head's layout is the other
+    // one, or a region holds more entries than its share, a second round trip
+    // loads exactly the live entries.
+    const int8_t path = sel_mode ? w.path[bh] : (int8_t)PATH_FALLBACK;
+    uint64_t e[EPT];
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) e[u] = 0ull;
+    const uint32_t cnt_r = lane < kCandRanges ? w.cand_cnt[(int64_t)bh * kCandRanges + lane] : 0u;
+    const uint32_t cnt_x = lane < (nreg_x < kFastRegions ? nreg_x : kFastRegions)
+                               ? w.surv_cnt[(int64_t)bh * a.n_regions + lane] : 0u;
+    bool reuse = sel_mode;
+    const uint64_t *base = reuse ? w.cand_ent + (int64_t)bh * kCandRanges * a.cand_cap
+                                 : w.surv + (int64_t)bh * a.row_stride;
+    int64_t stride = reuse ? a.cand_cap : kFilterRows;
+    int nreg = reuse ? kCandRanges : nreg_x;
+    if (nreg > kFastRegions) return false;
+    bool staged = false;
+    {
+        const int spec = (int)((kFastSlots / nreg < stride ? kFastSlots / nreg : stride) &
+                               ~(int64_t)(EPT - 1));
+        const int slot = tid * EPT;
+        const int rs = spec > 0 ? slot / spec : nreg;
+        const int js = slot - (rs < nreg ? rs : 0) * spec;
+        if (rs < nreg) {
+            const uint64_t *src = base + (int64_t)rs * stride + js;
+            if ((stride & 1) == 0) {
+                // 16-byte aligned: regions start on even entries, js is a multiple of EPT
+#pragma unroll
+                for (int u = 0; u < EPT / 2; ++u) {
+                    const uint4 x = ((const uint4 *)src)[u];
+                    e[2 * u] = ((uint64_t)x.y << 32) | x.x;
+                    e[2 * u + 1] = ((uint64_t)x.w << 32) | x.z;
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < EPT; ++u) e[u] = src[u];
+            }
+        }
+        const uint32_t rc = reuse ? cnt_r : cnt_x;
+        const bool fits = spec > 0 && __ballot(lane < nreg && rc > (uint32_t)spec) == 0ull;
+        if (sel_mode && path != PATH_REUSE) {
+            reuse = false;
+            base = w.surv + (int64_t)bh * a.row_stride;
+            stride = kFilterRows;
+            nreg = nreg_x;
+            if (nreg > kFastRegions) return false;
+        } else if (fits) {
+            // stage the speculative entries in index order
+            const uint32_t inc = wave_incl_scan(rc);
+            const uint32_t rpref = (uint32_t)__shfl((int)(inc - rc), rs < nreg ? rs : 0);
+            const uint32_t rcnt_s = (uint32_t)__shfl((int)rc, rs < nreg ? rs : 0);
+#pragma unroll
+            for (int u = 0; u < EPT; ++u)
+                if (rs < nreg && (uint32_t)(js + u) < rcnt_s) stage[rpref + js + u] = e[u];
+            staged = true;
+            __syncthreads();                                          // barrier 0
+        }
+    }
+    const uint32_t rcnt = reuse ? cnt_r : cnt_x;      // lane r: count of region r
+    const uint32_t incl = wave_incl_scan(rcnt);
+    const uint32_t n = (uint32_t)__builtin_amdgcn_readlane((int)incl, nreg - 1);
+    if (n == 0u) return false;
+    // p0: the index-order position of this thread's first entry; nlive: how many
+    // of its entries are live (they are the first ones)
+    uint32_t p0 = 0u, nlive = 0u;
+    if (staged) {
+        // the staged list is dense: thread t takes positions EPT*t .. EPT*t+EPT-1
+        p0 = (uint32_t)(tid * EPT);
+        nlive = p0 < n ? (n - p0 < (uint32_t)EPT ? n - p0 : (uint32_t)EPT) : 0u;
+#pragma unroll
+        for (int u = 0; u < EPT; ++u)
+            if ((uint32_t)u < nlive) e[u] = stage[p0 + u];
+    } else {
+        // region r gets ceil(count / EPT) threads, from thread start tincl[r] - need[r]
+        const uint32_t need = lane < nreg ? (rcnt + EPT - 1) / EPT : 0u;
+        const uint32_t tincl = wave_incl_scan(need);
+        const uint32_t tall = (uint32_t)__builtin_amdgcn_readlane((int)tincl, 63);
+        if (tall > (uint32_t)NT) return false;
+        int lo = 0;   // the last region whose thread start is <= tid
+#pragma unroll
+        for (int step = 32; step > 0; step >>= 1) {
+            const int c = lo + step;
+            const uint32_t st = (uint32_t)__shfl((int)(tincl - need), c < 64 ? c : 63);
+            if (c < nreg && st <= (uint32_t)tid) lo = c;
+        }
+        const uint32_t st0 = (uint32_t)__shfl((int)(tincl - need), lo);
+        const uint32_t rc = (uint32_t)__shfl((int)rcnt, lo);
+        const uint32_t j0 = ((uint32_t)tid - st0) * EPT;
+        if ((uint32_t)tid < tall && j0 < rc) {
+            p0 = (uint32_t)__shfl((int)(incl - rcnt), lo) + j0;
+            nlive = rc - j0 < (uint32_t)EPT ? rc - j0 : (uint32_t)EPT;
+            const uint64_t *src = base + (int64_t)lo * stride + j0;
+            if ((stride & 1) == 0) {
+#pragma unroll
+                for (int u = 0; u < EPT / 2; ++u) {
+                    if ((uint32_t)(2 * u) < nlive) {
+                        const uint4 x = ((const uint4 *)src)[u];
+                        e[2 * u] = ((uint64_t)x.y << 32) | x.x;
+                        e[2 * u + 1] = ((uint64_t)x.w << 32) | x.z;
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < EPT; ++u)
+                    if ((uint32_t)u < nlive) e[u] = src[u];
+            }
+        }
+    }
+    uint32_t valid = (1u << nlive) - 1u;   // bit u: entry u of this thread is a live entry
+    // waves holding no entry skip the per-entry work (a wave-uniform branch)
+    const bool wlive = __ballot(valid != 0u) != 0ull;
+
+    // the largest and smallest score key
+    uint32_t kmax = 0u, kmin = 0xFFFFFFFFu;
+    if (wlive) {
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            if ((valid >> u) & 1u) {
+                kmax = max(kmax, rank_key(e[u]));
+                kmin = min(kmin, rank_key(e[u]));
+            }
+        }
+    }
+    kmax = wave_max_u32(kmax);
+    kmin = ~wave_max_u32(~kmin);
+    if (lane == 0) {
+        fs.wmax[wave] = kmax;
+        fs.wmin[wave] = kmin;
+    }
+    __syncthreads();                                                  // barrier 1
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        kmax = max(kmax, fs.wmax[i]);
+        kmin = min(kmin, fs.wmin[i]);
+    }
+    const float smax = key_score(kmax), smin = key_score(kmin);
+    const int K = a.K;
+    const uint32_t kn = n < (uint32_t)K ? n : (uint32_t)K;
+
+    // Top-K (Eq. 1 / Eq. 11): the entries e >= thr.  Bins linear in the score
+    // between the smallest and the largest (monotone in the rank) locate the K-th
+    // largest in one bin; when that bin holds more than kTieMax entries, a second
+    // level of bins linear over the bin's own score range narrows it; the final
+    // bin's entries are ranked exactly by every wave.
+    uint64_t thr = 0ull;
+    if (n > (uint32_t)K) {
+        const float range = smax - smin;
+        if (!(range > 0.0f) || !(range < 3.0e38f)) return false;
+        float lo = smin, scale = (float)(kFastBins - 1) / range;
+        uint32_t cand = valid;     // entries still in the running
+        uint32_t k_rem = (uint32_t)K, cnt_b = 0u;
+        uint32_t above_mask = 0u;  // entries already known to be in the Top-K
+        for (int level = 0; level < 2; ++level) {
+            uint32_t bin[EPT];
+#pragma unroll
+            for (int u = 0; u < EPT; ++u) bin[u] = 0u;
+            if (wlive) {
+#pragma unroll
+                for (int u = 0; u < EPT; ++u) {
+                    bin[u] = (uint32_t)min(max((int)((key_score(rank_key(e[u])) - lo) * scale), 0),
+                                           kFastBins - 1);
+                    if ((cand >> u) & 1u) atomicAdd(&fs.hist[bin[u]], 1u);
+                }
+            }
+            __syncthreads();                                          // barrier 2
+            uint32_t bstar, above;
+            wave_find_bin<kFastBins>(fs.hist, k_rem, bstar, above, cnt_b);
+            uint32_t in_b = 0u;
+            if (wlive) {
+#pragma unroll
+                for (int u = 0; u < EPT; ++u) {
+                    if ((cand >> u) & 1u) {
+                        if (bin[u] > bstar) above_mask |= 1u << u;
+                        else if (bin[u] == bstar) in_b |= 1u << u;
+                    }
+                }
+            }
+            cand = in_b;
+            k_rem -= above;
+            if (cnt_b <= (uint32_t)kTieMax || level == 1) break;
+            // second level over the bin's score range (the bin's entries only)
+            __syncthreads();   // every wave has read the first-level histogram
+            for (int i = tid; i < kFastBins; i += NT) fs.hist[i] = 0u;
+            const float w0 = lo + (float)bstar / scale;
+            lo = w0;
+            scale = scale * (float)(kFastBins - 1);
+            __syncthreads();
+        }
+        if (cnt_b > (uint32_t)kTieMax) return false;
+        // the final bin's entries to LDS: one slot reservation per thread
+        if (wlive && cand != 0u) {
+            uint32_t at = atomicAdd(&fs.n_tie, (uint32_t)__popc(cand));
+#pragma unroll
+            for (int u = 0; u < EPT; ++u)
+                if ((cand >> u) & 1u) fs.tie[at++] = e[u];
+        }
+        __syncthreads();                                              // barrier 3
+        // every wave ranks the bin's entries (lane i holds entry i, the others are
+        // read as scalars): the k_rem-th largest is the threshold
+        const uint64_t x = lane < (int)cnt_b ? fs.tie[lane] : 0ull;
+        const uint32_t xlo = (uint32_t)x, xhi = (uint32_t)(x >> 32);
+        uint32_t higher = 0u;
+        for (int i = 0; i < (int)cnt_b; ++i) {
+            const uint32_t ylo = (uint32_t)__builtin_amdgcn_readlane((int)xlo, i);
+            const uint32_t yhi = (uint32_t)__builtin_amdgcn_readlane((int)xhi, i);
+            higher += (yhi > xhi || (yhi == xhi && ylo > xlo)) ? 1u : 0u;
+        }
+        const uint64_t at = __ballot(lane < (int)cnt_b && higher == k_rem - 1u);
+        const int tl = __builtin_ctzll(at);
+        thr = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)xhi, tl) << 32) |
+              (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)xlo, tl);
+        // selected: every entry above the final bin, and those of it at or above thr
+        if (wlive) {
+#pragma unroll
+            for (int u = 0; u < EPT; ++u)
+                if (((cand >> u) & 1u) && e[u] >= thr) above_mask |= 1u << u;
+        }
+        valid = above_mask;
+    }
+    const uint32_t selm = valid;
+    const uint32_t nsel = (uint32_t)__popc(selm);
+
+    // The selected entries in index order (the threads hold consecutive entries):
+    // each thread's position from a block scan of the per-thread counts, then the
+    // list in LDS, as (index << 32 | score key).
+    const uint32_t winc = wave_incl_scan(nsel);
+    if (lane == 63) fs.wsel[wave] = winc;
+    __syncthreads();                                                  // barrier 4
+    uint32_t pos = winc - nsel;
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) pos += ww < wave ? fs.wsel[ww] : 0u;
+    if (wlive) {
+#pragma unroll
+        for (int u = 0; u < EPT; ++u)
+            if ((selm >> u) & 1u) list[pos++] = ((uint64_t)rank_index(e[u]) << 32) | rank_key(e[u]);
+    }
+    __syncthreads();                                                  // barrier 5
+
+    // Eq. 12 on this block's slice: weights exp(s - max), the largest selected score
+    // being the largest of all.  LPR lanes per value row, RPW rows per wave
+    // instruction, four rows per lane in flight.
+    {
+        const int b = bh / a.Hq, g = (bh % a.Hq) / a.G;
+        const T *vbase = (const T *)a.v + ((int64_t)b * a.Hkv + g) * a.max_len * D + slice * DS;
+        const int sub = lane / LPR, vl = lane % LPR;
+        float acc[EPV], lsum = 0.0f;
+#pragma unroll
+        for (int i = 0; i < EPV; ++i) acc[i] = 0.0f;
+        for (int t0 = wave * RPW + sub; t0 < (int)kn; t0 += 4 * NW * RPW) {
+            uint4 raw[4];
+            float wt[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int t = t0 + q * NW * RPW;
+                const uint64_t se = list[t < (int)kn ? t : 0];
+                raw[q] = ((const uint4 *)(vbase + (int64_t)(uint32_t)(se >> 32) * D))[vl];
+                wt[q] = t < (int)kn ? expf(key_score((uint32_t)se) - smax) : 0.0f;
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                Dot<T>::axpy(raw[q], wt[q], acc);
+                lsum += vl == 0 ? wt[q] : 0.0f;
+            }
+        }
+        // sum over the lanes of each row that hold the same vl (row rotations), then
+        // over the rows of the block in LDS
+#pragma unroll
+        for (int o = LPR; o < 16; o <<= 1) {
+#pragma unroll
+            for (int i = 0; i < EPV; ++i) acc[i] += row_ror_f32(acc[i], o);
+            lsum += row_ror_f32(lsum, o);
+        }
+        const int row = wave * 4 + (lane >> 4);
+        if ((lane & 15) < LPR) {
+#pragma unroll
+            for (int i = 0; i < EPV; ++i) part[row][vl * EPV + i] = acc[i];
+            if (vl == 0) part[row][DS] = lsum;
+        }
+    }
+    __syncthreads();                                                  // barrier 6
+    if (tid < DS) {
+        float o = 0.0f, l = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 4 * NW; ++r) {
+            o += part[r][tid];
+            l += part[r][DS];
+        }
+        a.out[(int64_t)bh * D + slice * DS + tid] = o / l;
+    }
+
+    // which of the head's writes this block owns (shared out over its slices)
+    const bool own_sel = slice == 0, own_supp = (1 % kFinalSlices) == slice;
+    const bool own_qbar = (2 % kFinalSlices) == slice, own_misc = (3 % kFinalSlices) == slice;
+    const int64_t ent = (int64_t)bh * a.M + a.insert_slot;   // the cache entry written
+    auto put = [&](int32_t *dst) {
+        for (int t = tid; t < K; t += NT) dst[t] = t < (int)kn ? (int32_t)(list[t] >> 32) : -1;
+    };
+    if (own_sel) {
+        if (a.sel != nullptr) put(a.sel + (int64_t)bh * K);
+        if (a.dbg_ncand && tid == 0) a.dbg_ncand[bh] = reuse ? (int32_t)n : 0;
+        if (a.dbg_cand) {
+            int32_t *dc = a.dbg_cand + (int64_t)bh * a.cand_cap;
+            if (reuse) {
+#pragma unroll
+                for (int u = 0; u < EPT; ++u)
+                    if ((uint32_t)u < nlive) dc[p0 + u] = (int32_t)rank_index(e[u]);
+            }
+            for (int j = (reuse ? (int)n : 0) + tid; j < a.cand_cap; j += NT) dc[j] = -1;
+        }
+    }
+    if (a.do_insert) {
+        // Sec. 3.4: insert (q_bar, support) after either path
+        if (own_supp) {
+            put(w.supp + ent * K);
+            if (tid == 0) w.cnt[ent] = (int32_t)kn;
+        }
+        if (own_qbar) {
+            if (sel_mode) {
+                for (int t = tid; t < D; t += NT) w.qbar[ent * D + t] = w.qbar_cur[(int64_t)bh * D + t];
+            } else {
+                __shared__ float s_qbar[D];
+                __shared__ double s_red[NT / 64];
+                block_qbar<T, D, NT>((const T *)a.q + (int64_t)bh * a.q_head_stride, s_qbar, s_red);
+                for (int t = tid; t < D; t += NT) w.qbar[ent * D + t] = s_qbar[t];
+            }
+        }
+    }
+    if (own_misc) {
+        if (reuse) {
+            if (tid == 0) {
+                atomicAdd(&w.stats[STAT_CAND_SUM], (unsigned long long)n);
+                atomicMax(&w.stats[STAT_CAND_MAX], (unsigned long long)n);
+            }
+        } else {
+            // leave the histogram zeroed for the next launch
+            for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)bh * kHistBins + i] = 0u;
+        }
+    }
+    return true;
+}
+
 // kMulti: built for launches of several query positions (a.U > 1, the batched
 // prefill); the decode-step build keeps u = 0 out of its code.
 template <typename T, int D, bool kMulti>
@@ -1291,10 +1790,23 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     static_assert(SB % 16 == 0 && LPR >= 1 && LPR <= 64, "slice geometry");
     static_assert(kMaxRegions % NT == 0 && kCandRanges <= NT, "region ownership");
     __shared__ FinalSmem<D, NT> sm;
+    __shared__ FastSmem fs;
+    __shared__ float s_part[4 * (NT / 64)][DS + 1];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // the multi-position (prefill) build writes no output: one block per head
     constexpr int NS = kMulti ? 1 : kFinalSlices;
-    const int vh = blockIdx.x / NS, slice = blockIdx.x % NS;
+    int vh, slice;
+    if constexpr (kMulti) {
+        vh = blockIdx.x;
+        slice = 0;
+    } else {
+        // the NS blocks of head vh run on XCD vh % 8 (block j is placed on XCD
+        // j % 8), beside the range blocks that wrote the head's candidates
+        const int x = (int)blockIdx.x & 7, rest = (int)blockIdx.x >> 3;
+        slice = rest % NS;
+        vh = (rest / NS) * 8 + x;
+        if (vh >= a.B * a.Hq) return;
+    }
     const bool writes_out = a.out != nullptr && a.mode != MODE_PREFILL;
     if (slice != 0 && !writes_out) return;
     // Virtual head vh = u * B * Hq + bh: query position u of head bh (u = 0 unless
@@ -1312,6 +1824,10 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
         }
         if (a.dbg_ret)
             for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = -1;
+    }
+    if constexpr (!kMulti) {
+        if (writes_out && final_fast<T, D>(a, w, bh, slice, fs, sm.ent, sm.sel, s_part)) return;
+        __syncthreads();   // the general path follows the fast path's early exit
     }
 
     // Path, the region counts of both layouts and the first entries of every
@@ -2032,7 +2548,9 @@ template <typename T, int D>
 static void sim_desc(const StepArgs &a, KernelDesc *k)
 {
     const int nsb = (a.M + kSimSlots - 1) / kSimSlots;
-    *k = KernelDesc{(const void *)&k_sim<T, D>, dim3((unsigned)(a.B * a.Hq * nsb)), dim3(kSimThreads), 0u, 2};
+    // whole groups of 8 heads (one per XCD), nsb blocks each
+    *k = KernelDesc{(const void *)&k_sim<T, D>, dim3((unsigned)((a.B * a.Hq + 7) / 8 * 8 * nsb)),
+                    dim3(kSimThreads), 0u, 2};
 }
 
 template <typename T, int D, int G>
@@ -2053,9 +2571,11 @@ static void score_desc(const StepArgs &a, const Geometry &geo, KernelDesc *k)
 template <typename T, int D>
 static void final_desc(const StepArgs &a, KernelDesc *k)
 {
+    // decode build: whole groups of 8 heads (one per XCD), kFinalSlices blocks each
+    const unsigned blocks = a.U > 1 ? (unsigned)(a.B * a.Hq * a.U)
+                                    : (unsigned)((a.B * a.Hq + 7) / 8 * 8 * kFinalSlices);
     *k = KernelDesc{a.U > 1 ? (const void *)&k_final<T, D, true> : (const void *)&k_final<T, D, false>,
-                    dim3((unsigned)(a.B * a.Hq * a.U * (a.U > 1 ? 1 : kFinalSlices))),
-                    dim3(kFinalThreads), 0u, 2};
+                    dim3(blocks), dim3(kFinalThreads), 0u, 2};
 }
 
 // Group sizes run on the build for the next power of two (1, 2, 4 or 8); the
