@@ -18,13 +18,12 @@ constexpr int kSimThreads = 256;      // k_sim: 64 cached slots per block
 constexpr int kSimSlots = 64;
 constexpr int kScoreThreads = 512;    // k_score and k_filter blocks
 constexpr int kFinalThreads = 512;    // k_final blocks
-constexpr int kFinalSlices = 8;       // k_final blocks per head (one d-slice of V each)
 constexpr int kScanRowsPerIter = 128; // 8 waves x 16 rows
 constexpr int kCandRanges = 8;        // index ranges (k_score blocks) per reuse head
 constexpr int kCandList = 2048;       // candidates gathered per round in one range block
 constexpr int kSegWords = 2048;       // union bitmap segment: 65536 indices
 constexpr int kFilterRows = 4096;     // scores filtered per k_filter block
-constexpr int kEntCache = 8704;       // final-stage entries staged in LDS
+constexpr int kEntCache = 8192;       // final-stage entries staged in LDS
 constexpr int kMaxRegions = 4096;     // filter regions per head (max_len <= 16M)
 constexpr int kMaxK = 2048;
 constexpr int kMaxR = 32;

@@ -13,7 +13,7 @@
 //             an LDS bitmap and score those keys (Eq. 10).
 //   k_filter  per exact head, the scores at or above the histogram bin that holds
 //             the K-th largest, compacted in index order.
-//   k_final   kFinalSlices blocks per head: each selects the Top-K of the head's
+//   k_final   2, 4 or 8 blocks per head: each selects the Top-K of the head's
 //             candidates (Eq. 11) or surviving scores (Eq. 1) -- entries held in
 //             registers, value-linear score bins, the threshold bin ranked exactly
 //             (a radix select on 64-bit ranks for the heads that do not fit) --
@@ -116,6 +116,67 @@ __device__ __forceinline__ double quad_sum(double x)
 // Inclusive prefix sum over the 64 lanes of a wave: Hillis-Steele inside each row
 // of 16 lanes (DPP row shifts, lanes shifted in from outside the row read 0), then
 // the row totals carried across rows with the row broadcasts of lanes 15 and 31.
+// Reductions over a wave: DPP inside each row of 16 lanes (quad swaps, half-row
+// and row mirrors), then the four row results read as scalars.  Every lane gets
+// the result.
+__device__ __forceinline__ uint32_t row_max_u32(uint32_t x)
+{
+    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, kQuadXor1, 0xF, 0xF, true));
+    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, kQuadXor2, 0xF, 0xF, true));
+    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, kHalfMirror, 0xF, 0xF, true));
+    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x140, 0xF, 0xF, true));   // row_mirror
+    return x;
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x)
+{
+    x = row_max_u32(x);
+    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 0);
+    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 16);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 32);
+    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)x, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+__device__ __forceinline__ float wave_sum_f32(float x)
+{
+    x += dpp_f32<kQuadXor1>(x);
+    x += dpp_f32<kQuadXor2>(x);
+    x += dpp_f32<kHalfMirror>(x);
+    x += dpp_f32<0x140>(x);   // row_mirror
+    const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 0));
+    const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 16));
+    const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 32));
+    const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 48));
+    return (r0 + r1) + (r2 + r3);
+}
+
+__device__ __forceinline__ double wave_max_f64(double x)
+{
+    x = fmax(x, dpp_f64<kQuadXor1>(x));
+    x = fmax(x, dpp_f64<kQuadXor2>(x));
+    x = fmax(x, dpp_f64<kHalfMirror>(x));
+    x = fmax(x, dpp_f64<0x140>(x));   // row_mirror
+    auto rl = [&](int l) {
+        const uint64_t u = __builtin_bit_cast(uint64_t, x);
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+        return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+    };
+    return fmax(fmax(rl(0), rl(16)), fmax(rl(32), rl(48)));
+}
+
+// x from lane (i + n) mod 16 of the same row of 16 lanes (DPP row_ror:n, 1..15).
+__device__ __forceinline__ float row_ror_f32(float x, int n)
+{
+    int r;
+    switch (n) {
+    case 1: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x121, 0xF, 0xF, true); break;
+    case 2: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x122, 0xF, 0xF, true); break;
+    case 4: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x124, 0xF, 0xF, true); break;
+    default: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x128, 0xF, 0xF, true); break;
+    }
+    return __builtin_bit_cast(float, r);
+}
+
 __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x)
 {
     x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, false);  // row_shr:1
@@ -819,6 +880,7 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     const int xcd = cb & 7, rest = cb >> 3;
     const int s = rest % kCandRanges, bh = (rest / kCandRanges) * 8 + xcd;
     if (bh >= a.B * a.Hq) return;
+
     const int M = a.M;
     const int n_valid = (int)(a.n_ins < (int64_t)M ? a.n_ins : (int64_t)M);
     const int nsb = (M + kSimSlots - 1) / kSimSlots;
@@ -827,7 +889,6 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     int32_t *c_slot = (int32_t *)(lds + 8 * kCands);
     int32_t *c_cnt = (int32_t *)(lds + 12 * kCands);
     int32_t *c_age = (int32_t *)(lds + 16 * kCands);
-    int32_t *c_rank = (int32_t *)(lds + 20 * kCands);
     const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
 
     // Retrieved positions no list entry fills stay empty (possible only when the
@@ -855,7 +916,6 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
         c_rho[c] = use ? rr : -INFINITY;
         c_cnt[c] = use ? cn : 0;
         c_age[c] = use ? slot_age(age0, sl, M) : 0x7FFFFFFF;
-        c_rank[c] = 0;
     }
     uint4 qv[R::kNV];
     {
@@ -865,46 +925,34 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     }
     __syncthreads();
 
-    // Eq. 7: merge the blocks' Top-R lists.  The global rank of candidate c is
-    // its position in its own list plus, for every other list, the number of
-    // entries that are more similar, or equally similar and newer (for recent-R
-    // retrieval: that are newer); one thread counts one (candidate, list) pair.
-    for (int pr = tid; pr < nc * nsb; pr += NT) {
-        const int c = pr / nsb, o = pr - c * nsb;
-        const int32_t sl = c_slot[c];
-        if (sl < 0 || o == c / per) continue;
-        const double rc = c_rho[c];
-        const int ac = c_age[c];
-        // Invalid entries carry rho = -inf and never count.  All reads of a
-        // chunk are issued before any comparison.
-        int cnt = 0;
-        for (int k0 = 0; k0 < per; k0 += 4) {
-            double rr[4];
-            int aa[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int e = o * per + (k0 + u < per ? k0 + u : per - 1);
-                rr[u] = c_rho[e];
-                aa[u] = c_age[e];
+    // Eq. 7: merge the blocks' Top-R lists (each sorted best first) in one wave:
+    // lane o holds the head of list o, and each round the best head (the most
+    // similar, then the newer; for recent-R retrieval the newer) is retrieved and
+    // its list advances.  Heads that compare with nothing (non-finite similarity)
+    // are never taken, and the round ends the merge when no head is left.
+    if (wave == 0) {
+        const bool recent = a.retrieval == 1;
+        int ptr = 0;
+        for (int k = 0; k < nret_all; ++k) {
+            const int e = lane * per + (ptr < per ? ptr : per - 1);
+            const bool live = lane < nsb && ptr < per && c_slot[e] >= 0;
+            const double rh = live ? c_rho[e] : -INFINITY;
+            const uint32_t ah = live ? (uint32_t)c_age[e] : 0xFFFFFFFFu;
+            bool cand = live;
+            if (!recent) {
+                const double m = wave_max_f64(rh);
+                cand = live && rh == m;
             }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const bool beats = a.retrieval == 1 ? (aa[u] < ac)
-                                                    : ((rr[u] > rc) | ((rr[u] == rc) & (aa[u] < ac)));
-                cnt += (beats & (k0 + u < per)) ? 1 : 0;
+            const uint32_t amin = ~wave_max_u32(cand ? ~ah : 0u);
+            const uint64_t win = __ballot(cand && ah == amin);
+            if (win == 0ull) break;
+            const int wl = __builtin_ctzll(win);
+            if (lane == wl) {
+                s_ret[k] = c_slot[e];
+                s_retcnt[k] = c_cnt[e];
+                s_retrho[k] = rh;
+                ++ptr;
             }
-        }
-        if (cnt) atomicAdd(&c_rank[c], cnt);
-    }
-    __syncthreads();
-    for (int c = tid; c < nc; c += NT) {
-        const int32_t sl = c_slot[c];
-        if (sl < 0) continue;
-        const int rank = c - (c / per) * per + c_rank[c];
-        if (rank < nret_all) {
-            s_ret[rank] = sl;
-            s_retcnt[rank] = c_cnt[c];
-            s_retrho[rank] = c_rho[c];
         }
     }
     __syncthreads();
@@ -1127,13 +1175,13 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
 constexpr int kTieMax = 64;        // bin sizes resolved by one wave
 constexpr int kSpecLoads = 4;      // speculative entry loads per thread
 
-template <int D, int NT>
+template <int D, int DS, int NT>
 struct FinalSmem {
     uint64_t ent[kEntCache];        // the head's entries in index order, when they fit
     uint64_t sel[kMaxK];            // selected (index << 32 | score key), index order
     uint32_t pref[kMaxRegions + 1]; // region prefix counts
     uint32_t hist[kHistBins];
-    float part[NT / 64][D / kFinalSlices];
+    float part[NT / 64][DS];
     float lpart[NT / 64];
     float qbar[D];
     double red64[NT / 64];
@@ -1169,8 +1217,8 @@ struct Regions {
 // Descending scan of sm.hist (nb <= kHistBins bins): the bin where the count
 // from the top reaches k (found_digit), the count above it and its own count.
 // Thread t covers bins nb-1-BPT*t .. nb-BPT-BPT*t.
-template <int D, int NT>
-__device__ void find_bin(FinalSmem<D, NT> &sm, uint32_t nb, uint32_t k)
+template <class SM, int NT>
+__device__ void find_bin(SM &sm, uint32_t nb, uint32_t k)
 {
     constexpr int BPT = (kHistBins + NT - 1) / NT;
     const int tid = threadIdx.x;
@@ -1199,8 +1247,8 @@ __device__ void find_bin(FinalSmem<D, NT> &sm, uint32_t nb, uint32_t k)
 // first, starting at the highest bit in which the ranks differ (rmax ^ rmin).
 // On return the top min(K, n) entries are exactly those with
 // (rank & mask) >= prefix (mask == 0 selects everything).
-template <int D, int NT>
-__device__ void radix_threshold(const Regions &rg, int K, FinalSmem<D, NT> &sm, uint64_t &prefix,
+template <class SM, int NT>
+__device__ void radix_threshold(const Regions &rg, int K, SM &sm, uint64_t &prefix,
                                 uint64_t &mask)
 {
     const int tid = threadIdx.x;
@@ -1225,7 +1273,7 @@ __device__ void radix_threshold(const Regions &rg, int K, FinalSmem<D, NT> &sm, 
             if ((e & mask) == prefix) atomicAdd(&sm.hist[(uint32_t)(e >> sh) & (nb - 1u)], 1u);
         }
         __syncthreads();
-        find_bin<D, NT>(sm, nb, k_rem);
+        find_bin<SM, NT>(sm, nb, k_rem);
         k_rem -= sm.found_above;
         prefix |= (uint64_t)sm.found_digit << sh;
         mask |= (uint64_t)(nb - 1u) << sh;
@@ -1242,8 +1290,8 @@ __device__ void radix_threshold(const Regions &rg, int K, FinalSmem<D, NT> &sm, 
 // every entry of a lower one); the K-th largest then lies in one bin, whose
 // entries one wave ranks exactly when there are at most kTieMax of them.  Returns
 // false when that bin is larger (heavy ties), leaving the radix select to decide.
-template <int D, int NT>
-__device__ bool value_threshold(const uint64_t *ent, int n, int K, FinalSmem<D, NT> &sm,
+template <class SM, int NT>
+__device__ bool value_threshold(const uint64_t *ent, int n, int K, SM &sm,
                                 uint64_t &thr)
 {
     const int tid = threadIdx.x, lane = tid & 63;
@@ -1266,7 +1314,7 @@ __device__ bool value_threshold(const uint64_t *ent, int n, int K, FinalSmem<D, 
             if (j0 + u * NT < n) atomicAdd(&sm.hist[bin_of(e[u])], 1u);
     }
     __syncthreads();
-    find_bin<D, NT>(sm, kHistBins, (uint32_t)K);
+    find_bin<SM, NT>(sm, kHistBins, (uint32_t)K);
     const uint32_t bstar = sm.found_digit, cnt = sm.found_cnt;
     const uint32_t k_rem = (uint32_t)K - sm.found_above;
     if (cnt > (uint32_t)kTieMax) return false;
@@ -1303,57 +1351,10 @@ __device__ bool value_threshold(const uint64_t *ent, int n, int K, FinalSmem<D, 
 // of bins) take the general path below, which reloads everything.
 // ---------------------------------------------------------------------------
 
-constexpr int kFastEPT = 8;                            // consecutive entries per thread
-constexpr int kFastSlots = kFinalThreads * kFastEPT;   // entries one block holds
+
 constexpr int kFastBins = 512;                         // value-linear score bins
 constexpr int kFastRegions = 64;                       // regions one wave ranks
 
-
-// Reductions over a wave: DPP inside each row of 16 lanes (quad swaps, half-row
-// and row mirrors), then the four row results read as scalars.  Every lane gets
-// the result.
-__device__ __forceinline__ uint32_t row_max_u32(uint32_t x)
-{
-    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, kQuadXor1, 0xF, 0xF, true));
-    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, kQuadXor2, 0xF, 0xF, true));
-    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, kHalfMirror, 0xF, 0xF, true));
-    x = max(x, (uint32_t)__builtin_amdgcn_mov_dpp((int)x, 0x140, 0xF, 0xF, true));   // row_mirror
-    return x;
-}
-__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x)
-{
-    x = row_max_u32(x);
-    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)x, 0);
-    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 16);
-    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)x, 32);
-    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)x, 48);
-    return max(max(r0, r1), max(r2, r3));
-}
-__device__ __forceinline__ float wave_sum_f32(float x)
-{
-    x += dpp_f32<kQuadXor1>(x);
-    x += dpp_f32<kQuadXor2>(x);
-    x += dpp_f32<kHalfMirror>(x);
-    x += dpp_f32<0x140>(x);   // row_mirror
-    const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 0));
-    const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 16));
-    const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 32));
-    const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 48));
-    return (r0 + r1) + (r2 + r3);
-}
-
-// x from lane (i + n) mod 16 of the same row of 16 lanes (DPP row_ror:n, 1..15).
-__device__ __forceinline__ float row_ror_f32(float x, int n)
-{
-    int r;
-    switch (n) {
-    case 1: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x121, 0xF, 0xF, true); break;
-    case 2: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x122, 0xF, 0xF, true); break;
-    case 4: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x124, 0xF, 0xF, true); break;
-    default: r = __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x128, 0xF, 0xF, true); break;
-    }
-    return __builtin_bit_cast(float, r);
-}
 
 struct FastSmem {
     uint32_t hist[kFastBins];
@@ -1404,14 +1405,16 @@ __device__ __forceinline__ void wave_find_bin(const uint32_t *hist, uint32_t k, 
     cnt = (uint32_t)__builtin_amdgcn_readlane((int)cb, src);
 }
 
-// Block (bh, slice) of k_final on the fast path.  Returns false, with every thread
+// Block (bh, slice) of k_final on the fast path, one of NS slice blocks of the
+// head, holding up to EPT entries per thread.  Returns false, with every thread
 // agreeing and nothing written yet, when the head must take the general path.
-template <typename T, int D>
+template <typename T, int D, int NS, int EPT>
 __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, FastSmem &fs,
-                           uint64_t *stage, uint64_t *list, float (*part)[D / kFinalSlices + 1])
+                           uint64_t *stage, uint64_t *list, float (*part)[D / NS + 1])
 {
-    constexpr int NT = kFinalThreads, NW = NT / 64, EPT = kFastEPT;
-    constexpr int DS = D / kFinalSlices;                  // elements of this block's slice
+    constexpr int NT = kFinalThreads, NW = NT / 64;
+    constexpr int kFastSlots = NT * EPT;                  // entries one block holds
+    constexpr int DS = D / NS;                            // elements of this block's slice
     constexpr int EPV = 16 / (int)sizeof(T);
     constexpr int LPR = DS * (int)sizeof(T) / 16;         // lanes per slice row
     constexpr int RPW = 64 / LPR;                         // rows per wave instruction
@@ -1724,8 +1727,8 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
     }
 
     // which of the head's writes this block owns (shared out over its slices)
-    const bool own_sel = slice == 0, own_supp = (1 % kFinalSlices) == slice;
-    const bool own_qbar = (2 % kFinalSlices) == slice, own_misc = (3 % kFinalSlices) == slice;
+    const bool own_sel = slice == 0, own_supp = (1 % NS) == slice;
+    const bool own_qbar = (2 % NS) == slice, own_misc = (3 % NS) == slice;
     const int64_t ent = (int64_t)bh * a.M + a.insert_slot;   // the cache entry written
     auto put = [&](int32_t *dst) {
         for (int t = tid; t < K; t += NT) dst[t] = t < (int)kn ? (int32_t)(list[t] >> 32) : -1;
@@ -1776,12 +1779,14 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
 
 // kMulti: built for launches of several query positions (a.U > 1, the batched
 // prefill); the decode-step build keeps u = 0 out of its code.
-template <typename T, int D, bool kMulti>
+template <typename T, int D, bool kMulti, int NSL, int EPT>
 __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
 {
     constexpr int NT = kFinalThreads;
     constexpr int NW = NT / 64;
-    constexpr int DS = D / kFinalSlices;                 // elements per slice
+    // the multi-position (prefill) build writes no output: one block per head
+    constexpr int NS = kMulti ? 1 : NSL;
+    constexpr int DS = D / NSL;                          // elements per slice
     constexpr int SB = DS * (int)sizeof(T);              // bytes per slice row
     constexpr int LPR = SB / 16;                         // lanes per slice row
     constexpr int RPW = 64 / LPR;                        // rows per wave instruction
@@ -1789,12 +1794,11 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     constexpr int kRegPerThread = kMaxRegions / NT;
     static_assert(SB % 16 == 0 && LPR >= 1 && LPR <= 64, "slice geometry");
     static_assert(kMaxRegions % NT == 0 && kCandRanges <= NT, "region ownership");
-    __shared__ FinalSmem<D, NT> sm;
+    __shared__ FinalSmem<D, DS, NT> sm;
     __shared__ FastSmem fs;
     __shared__ float s_part[4 * (NT / 64)][DS + 1];
+    static_assert(NT * EPT <= kEntCache, "the fast path stages its entries in sm.ent");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // the multi-position (prefill) build writes no output: one block per head
-    constexpr int NS = kMulti ? 1 : kFinalSlices;
     int vh, slice;
     if constexpr (kMulti) {
         vh = blockIdx.x;
@@ -1826,7 +1830,8 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
             for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = -1;
     }
     if constexpr (!kMulti) {
-        if (writes_out && final_fast<T, D>(a, w, bh, slice, fs, sm.ent, sm.sel, s_part)) return;
+        if (writes_out && final_fast<T, D, NS, EPT>(a, w, bh, slice, fs, sm.ent, sm.sel, s_part))
+            return;
         __syncthreads();   // the general path follows the fast path's early exit
     }
 
@@ -1981,10 +1986,10 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     uint64_t thr = 0ull;
     if (rg.n > a.K) {
         bool done = false;
-        if (rg.staged) done = value_threshold<D, NT>(rg.staged, rg.n, a.K, sm, thr);
+        if (rg.staged) done = value_threshold<FinalSmem<D, DS, NT>, NT>(rg.staged, rg.n, a.K, sm, thr);
         if (!done) {
             uint64_t prefix, mask;
-            radix_threshold<D, NT>(rg, a.K, sm, prefix, mask);
+            radix_threshold<FinalSmem<D, DS, NT>, NT>(rg, a.K, sm, prefix, mask);
             thr = mask == 0ull ? 0ull : prefix;
         }
     }
@@ -2568,14 +2573,31 @@ static void score_desc(const StepArgs &a, const Geometry &geo, KernelDesc *k)
     }
 }
 
+// k_final's geometry for a decode launch: slices per head so that the launch has
+// about 256 blocks (one per CU; each block takes most of a CU's LDS), and 16
+// entries per thread where a head's candidate cap is well past 4096 entries.
+int final_slices(const StepArgs &a)
+{
+    const int bh = a.B * a.Hq;
+    return bh <= 32 ? 8 : (bh <= 64 ? 4 : 2);
+}
+int final_ept(const StepArgs &a) { return (int64_t)a.R * a.K + a.W > 4608 ? 16 : 8; }
+
 template <typename T, int D>
 static void final_desc(const StepArgs &a, KernelDesc *k)
 {
-    // decode build: whole groups of 8 heads (one per XCD), kFinalSlices blocks each
-    const unsigned blocks = a.U > 1 ? (unsigned)(a.B * a.Hq * a.U)
-                                    : (unsigned)((a.B * a.Hq + 7) / 8 * 8 * kFinalSlices);
-    *k = KernelDesc{a.U > 1 ? (const void *)&k_final<T, D, true> : (const void *)&k_final<T, D, false>,
-                    dim3(blocks), dim3(kFinalThreads), 0u, 2};
+    if (a.U > 1) {
+        *k = KernelDesc{(const void *)&k_final<T, D, true, 8, 8>, dim3((unsigned)(a.B * a.Hq * a.U)),
+                        dim3(kFinalThreads), 0u, 2};
+        return;
+    }
+    const int ns = final_slices(a), ept = final_ept(a);
+    const void *f;
+    if (ns == 8) f = ept == 8 ? (const void *)&k_final<T, D, false, 8, 8> : (const void *)&k_final<T, D, false, 8, 16>;
+    else if (ns == 4) f = ept == 8 ? (const void *)&k_final<T, D, false, 4, 8> : (const void *)&k_final<T, D, false, 4, 16>;
+    else f = ept == 8 ? (const void *)&k_final<T, D, false, 2, 8> : (const void *)&k_final<T, D, false, 2, 16>;
+    // whole groups of 8 heads (one per XCD), ns blocks each
+    *k = KernelDesc{f, dim3((unsigned)((a.B * a.Hq + 7) / 8 * 8 * ns)), dim3(kFinalThreads), 0u, 2};
 }
 
 // Group sizes run on the build for the next power of two (1, 2, 4 or 8); the
