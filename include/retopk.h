@@ -115,10 +115,15 @@ typedef struct {
 
 /* Create a handle: validates cfg and allocates the caches (C entries of d floats
  * and K indices per query head, Eq. 5, metadata cost of Sec. 3.5) and the step
- * workspaces on the current HIP device.  The cache starts empty. */
+ * workspaces on the current HIP device.  The cache starts empty.  It takes no
+ * stream on purpose: it allocates and clears its memory synchronously and
+ * returns only once the device has finished, so it is ordered before every later
+ * call of the handle on any stream. */
 retopk_status retopk_create(const retopk_config *cfg, retopk_handle *out);
 
-/* Release everything retopk_create allocated.  NULL is accepted. */
+/* Release everything retopk_create allocated: the per-head caches and the
+ * preallocated step workspaces of Sec. 3.5.  Waits for the device first.  NULL is
+ * accepted. */
 retopk_status retopk_destroy(retopk_handle h);
 
 /* Cache initialisation from the prompt tail (Sec. 3.3): q_tail holds the queries
@@ -199,7 +204,11 @@ retopk_status exact_topk_attention_noalloc(const retopk_config *cfg, const void 
                                            const void *k, const void *v, int64_t len,
                                            float *out, int32_t *sel, void *stream);
 
-/* Read the cumulative counters (synchronises). */
+/* Read the cumulative counters (synchronises): head-steps per path of Eq. 13 --
+ * the path mix of Sec. 4.2 (reuse / fallback / refresh shares), the reuse share
+ * of Table 2 and the exact-path share of the component ablation (Table 3) -- the
+ * full-history scans the exact path ran, and the candidate-set sizes, bounded by
+ * Eq. 14. */
 retopk_status retopk_stats(retopk_handle h, retopk_stats_t *out);
 
 /* Copy the cache state to host arrays (synchronises):

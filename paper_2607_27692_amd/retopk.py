@@ -30,9 +30,26 @@ EXPORTS = ("retopk_create", "retopk_destroy", "retopk_prefill_init", "retopk_dec
 
 
 class RetopkError(RuntimeError):
-    def __init__(self, fn: str, code: int):
-        super().__init__(f"{fn}: {STATUS.get(code, code)} ({code})")
+    def __init__(self, fn: str, code: int, detail: str = ""):
+        super().__init__(f"{fn}: {STATUS.get(code, code)} ({code})" + (f": {detail}" if detail else ""))
         self.code = code
+
+
+def _check_tensor(fn: str, name: str, x, numel: int, itemsize: int):
+    """A torch tensor argument must be on the GPU, contiguous, of the element size
+    the call expects and at least as large as the layout the call indexes; the
+    call is refused (RETOPK_ERR_ARG) before reaching the library otherwise.  Raw
+    addresses (ints) and None pass unchecked."""
+    if x is None or isinstance(x, int) or not hasattr(x, "is_cuda"):
+        return
+    if not x.is_cuda:
+        raise RetopkError(fn, -1, f"{name} is not a GPU tensor")
+    if not x.is_contiguous():
+        raise RetopkError(fn, -1, f"{name} is not contiguous")
+    if x.element_size() != itemsize:
+        raise RetopkError(fn, -1, f"{name} has {x.element_size()}-byte elements, {itemsize} expected")
+    if x.numel() < numel:
+        raise RetopkError(fn, -1, f"{name} has {x.numel()} elements, {numel} expected")
 
 
 class retopk_config(C.Structure):
@@ -165,6 +182,7 @@ def exact_topk_attention(h, q, k, v, length, out, sel=None, stream=None) -> None
 def exact_topk_attention_noalloc(cfg: retopk_config, q, k, v, length, out, sel=None,
                                  stream=None) -> None:
     """exact_topk_attention without a handle, on the library's fixed scratch."""
+    _check_io("exact_topk_attention_noalloc", _cfg_dict(cfg), q=q, k=k, v=v, out=out, sel=sel)
     _check("exact_topk_attention_noalloc", load().exact_topk_attention_noalloc(
         C.byref(cfg), _addr(q), _addr(k), _addr(v), length, _addr(out), _addr(sel),
         _stream(stream)))
@@ -229,6 +247,28 @@ def retopk_status_string(code: int) -> str:
     return load().retopk_status_string(code).decode()
 
 
+def _cfg_dict(cfg: retopk_config) -> dict:
+    return {n: getattr(cfg, n) for n, _ in retopk_config._fields_}
+
+
+def _check_io(fn: str, c: dict, q=None, k=None, v=None, out=None, sel=None, q_tail=None,
+              n_tail: int = 0):
+    """Layout checks of the tensor arguments against the configuration c (see
+    include/retopk.h: q [B, Hq, d], k and v [B, Hkv, max_len, d], out [B, Hq, d]
+    float32, sel [B, Hq, K] int32, q_tail [B, Hq, n, d])."""
+    dt = c["dtype"]
+    es = 2 if dt in ("bf16", RETOPK_BF16) else 4
+    bhq = c["batch"] * c["n_q_heads"]
+    d = c["head_dim"]
+    _check_tensor(fn, "q", q, bhq * d, es)
+    kv = c["batch"] * c["n_kv_heads"] * c["max_len"] * d
+    _check_tensor(fn, "k", k, kv, es)
+    _check_tensor(fn, "v", v, kv, es)
+    _check_tensor(fn, "out", out, bhq * d, 4)
+    _check_tensor(fn, "sel", sel, bhq * c["k"], 4)
+    _check_tensor(fn, "q_tail", q_tail, bhq * n_tail * d, es)
+
+
 # ---------------------------------------------------------------------------
 # Convenience wrapper
 # ---------------------------------------------------------------------------
@@ -258,15 +298,19 @@ class Handle:
             pass
 
     def prefill_init(self, q_tail, n, k, v, prefill_len, stream=None):
+        _check_io("retopk_prefill_init", self.cfg, k=k, v=v, q_tail=q_tail, n_tail=n)
         retopk_prefill_init(self.h, q_tail, n, k, v, prefill_len, stream)
 
     def decode_step(self, q, k, v, length, out, sel=None, dbg=None, stream=None):
+        _check_io("retopk_decode_step", self.cfg, q=q, k=k, v=v, out=out, sel=sel)
         retopk_decode_step(self.h, q, k, v, length, out, sel, dbg, stream)
 
     def exact(self, q, k, v, length, out, sel=None, stream=None):
+        _check_io("exact_topk_attention", self.cfg, q=q, k=k, v=v, out=out, sel=sel)
         exact_topk_attention(self.h, q, k, v, length, out, sel, stream)
 
     def full(self, q, k, v, length, out, stream=None):
+        _check_io("full_attention", self.cfg, q=q, k=k, v=v, out=out)
         full_attention(self.h, q, k, v, length, out, stream)
 
     def stats(self):
@@ -283,6 +327,15 @@ class Handle:
         return dict(qbar=qbar, supp=supp, cnt=cnt, n_inserted=n_ins, t_dec=t_dec)
 
     def set_state(self, qbar, supp, cnt, n_inserted, t_dec):
+        import numpy as np
+        c = self.cfg
+        bh = c["batch"] * c["n_q_heads"]
+        want = {"qbar": (bh, c["cache_cap"], c["head_dim"]), "supp": (bh, c["cache_cap"], c["k"]),
+                "cnt": (bh, c["cache_cap"])}
+        for name, arr in (("qbar", qbar), ("supp", supp), ("cnt", cnt)):
+            if tuple(np.shape(arr)) != want[name]:
+                raise RetopkError("retopk_set_state", -1,
+                                  f"{name} has shape {tuple(np.shape(arr))}, {want[name]} expected")
         retopk_set_state(self.h, qbar, supp, cnt, n_inserted, t_dec)
 
     def profile(self, enable=True):

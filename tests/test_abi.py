@@ -118,3 +118,40 @@ def test_noalloc_workspace_formula():
     limit = 64 << 20
     assert need(32, 131328) <= limit < need(128, 65792)
     assert abs(need(32, 131328) / 1e6 - 52.2) < 0.1
+
+
+class _FakeTensor:
+    """Stands in for a torch tensor in the binding's argument checks."""
+    def __init__(self, numel, itemsize, cuda=True, contiguous=True):
+        self.is_cuda, self._n, self._i, self._c = cuda, numel, itemsize, contiguous
+
+    def numel(self):
+        return self._n
+
+    def element_size(self):
+        return self._i
+
+    def is_contiguous(self):
+        return self._c
+
+
+def test_binding_checks_tensor_layouts():
+    """The Python binding refuses tensors that are on the host, not contiguous, of the
+    wrong element size or smaller than the layout the call indexes, before calling
+    the library (RETOPK_ERR_ARG); raw addresses pass through to the library's own
+    checks."""
+    c = dict(batch=1, n_q_heads=4, n_kv_heads=2, head_dim=64, max_len=100, k=8, dtype="bf16")
+    ok = dict(q=_FakeTensor(4 * 64, 2), k=_FakeTensor(2 * 100 * 64, 2),
+              v=_FakeTensor(2 * 100 * 64, 2), out=_FakeTensor(4 * 64, 4), sel=_FakeTensor(32, 4))
+    R._check_io("f", c, **ok)
+    R._check_io("f", c, q=16, k=16, v=16, out=16, sel=None)     # raw addresses
+    for name, bad in (("q", _FakeTensor(4 * 64, 2, cuda=False)),
+                      ("k", _FakeTensor(2 * 100 * 64, 2, contiguous=False)),
+                      ("v", _FakeTensor(2 * 100 * 64, 4)),
+                      ("out", _FakeTensor(4 * 64 - 1, 4)),
+                      ("sel", _FakeTensor(31, 4))):
+        with pytest.raises(R.RetopkError) as e:
+            R._check_io("f", c, **dict(ok, **{name: bad}))
+        assert e.value.code == -1 and name in str(e.value)
+    with pytest.raises(R.RetopkError):
+        R._check_io("f", c, q_tail=_FakeTensor(4 * 3 * 64 - 1, 2), n_tail=3)

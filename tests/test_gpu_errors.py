@@ -39,8 +39,14 @@ def test_errors_leave_the_handle_usable():
         h.decode_step(q_dec[1], k, v, w.step_len(0) - 1, out, sel)
     assert _status(e) == -5
     misaligned = out.view(-1)[1:]                    # a 4-byte offset
-    with pytest.raises(R.RetopkError) as e:
+    with pytest.raises(R.RetopkError) as e:          # refused by the binding (too small)
         h.decode_step(q_dec[1], k, v, w.step_len(1), misaligned, sel)
+    assert _status(e) == -1
+    with pytest.raises(R.RetopkError) as e:          # and, as a raw address, by the library
+        R.retopk_decode_step(h.h, q_dec[1], k, v, w.step_len(1), misaligned.data_ptr(), sel)
+    assert _status(e) == -1
+    with pytest.raises(R.RetopkError) as e:          # a host tensor never reaches the library
+        h.decode_step(q_dec[1].cpu(), k, v, w.step_len(1), out, sel)
     assert _status(e) == -1
     with pytest.raises(R.RetopkError) as e:
         h.exact(q_dec[1], k, v, w.max_len + 1, out, sel)
