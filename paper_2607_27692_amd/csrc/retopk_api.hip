@@ -113,15 +113,19 @@ Geometry step_geometry(const retopk_config &c, int64_t len, int mode)
     const int64_t rows = (int64_t)c.batch * c.n_kv_heads * len;
     const int64_t want = ceil_div(rows, 2 * kScanRowsPerIter);
     // In MODE_SELECT the scan shares the launch with the range blocks and covers
-    // only the groups with a fallback head: a fixed number of blocks per KV group,
-    // so that a step where most groups fall back still spreads over the chip.
-    int64_t sel_cap = (int64_t)kScanBlocksPerGroup * c.batch * c.n_kv_heads;
-    sel_cap = sel_cap < kScanBlocksSelect ? kScanBlocksSelect
-                                          : (sel_cap > kScanBlocksExact ? kScanBlocksExact : sel_cap);
-    const int cap = mode == MODE_SELECT ? (int)sel_cap : kScanBlocksExact;
+    // only the groups with a fallback head: one scan block per CU, rounded to
+    // whole groups of 8 so that the range blocks' XCD placement is kept whichever
+    // kind comes first.
+    const int cap = mode == MODE_SELECT ? kScanBlocksSelect : kScanBlocksExact;
     g.scan_blocks = (int)(want < cap ? want : cap);
+    if (mode == MODE_SELECT) g.scan_blocks = (g.scan_blocks + 7) / 8 * 8;
     // range blocks: whole groups of 8 heads (one head per XCD)
     g.cand_blocks = mode == MODE_SELECT ? (int)((heads_of(c) + 7) / 8 * 8 * kCandRanges) : 0;
+    // When the range blocks need more than one block slot per CU, the scan blocks
+    // go first, so that they hold a slot on every CU from the start instead of
+    // waiting for the range blocks to drain; otherwise the range blocks, which
+    // carry the step's critical path, go first.
+    g.scan_first = g.cand_blocks > kCUs;
     g.filter_blocks_per_head = (int)ceil_div(len, kFilterRows);
     return g;
 }
@@ -431,6 +435,10 @@ retopk_status retopk_decode_step(retopk_handle h, const void *q, const void *k, 
 
     StepArgs a = base_args(h);
     a.mode = mode;
+    // Scan-fed candidates pay off when the scan blocks run beside the range blocks
+    // from the start (see step_geometry); otherwise the group check would only
+    // lengthen the range blocks.
+    a.scan_fed = mode == MODE_SELECT && step_geometry(c, len, mode).scan_first ? 1 : 0;
     a.q = q;
     a.k = k;
     a.v = v;

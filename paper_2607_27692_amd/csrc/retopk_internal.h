@@ -29,8 +29,8 @@ constexpr int kMaxK = 2048;
 constexpr int kMaxR = 32;
 constexpr int kMaxCache = 4096;
 constexpr int kMaxHeads = 2048;       // B * Hq
-constexpr int kScanBlocksSelect = 256;  // k_score scan blocks in MODE_SELECT: at least this,
-constexpr int kScanBlocksPerGroup = 32; // or this many per KV group (capped at kScanBlocksExact)
+constexpr int kCUs = 256;               // compute units of the chip
+constexpr int kScanBlocksSelect = kCUs; // k_score scan blocks in MODE_SELECT (one per CU)
 constexpr int kScanBlocksExact = 2048;  // k_score scan blocks when every head is exact
 constexpr int64_t kMaxLen = (int64_t)kMaxRegions * kFilterRows;
 
@@ -52,8 +52,11 @@ enum Mode : int {
     MODE_PREFILL = 4    // prefill initialisation: insert only, no output
 };
 
-// Path codes (same values as retopk_path).
-enum : int8_t { PATH_REUSE = 0, PATH_FALLBACK = 1, PATH_REFRESH = 2, PATH_COLD = 3 };
+// Path codes (same values as retopk_path).  PATH_REUSE_SCANNED (internal, never
+// reported): a reuse head whose KV group is scanned in the same step for another
+// head's fallback; its candidates take their scores from that scan.
+enum : int8_t { PATH_REUSE = 0, PATH_FALLBACK = 1, PATH_REFRESH = 2, PATH_COLD = 3,
+                PATH_REUSE_SCANNED = 4 };
 
 // Device counters (uint64) behind retopk_stats.
 enum : int {
@@ -98,6 +101,8 @@ struct StepArgs {
     int retrieval;             // 0: R most similar entries (Eq. 7); 1: R most recent
     float inv_sqrt_d;          // fl32(1 / sqrt(d))
     int mode;
+    int scan_fed;              // MODE_SELECT: the reuse heads of a scanned KV group take
+                               // their candidates' scores from the scan (PATH_REUSE_SCANNED)
     const void *q;             // element (b, h, e) at q[(b*Hq + h) * q_head_stride + e]
     int64_t q_head_stride;
     const void *k;
@@ -124,6 +129,7 @@ struct StepArgs {
 struct Geometry {
     int scan_blocks;           // scan blocks of k_score (they split the scanned rows)
     int cand_blocks;           // ceil(B * Hq / 8) * 8 * kCandRanges in MODE_SELECT, else 0
+    int scan_first;            // k_score's scan blocks come before its range blocks
     int filter_blocks_per_head;
     // batched prefill (k_pf_score): (KV group, key chunk) pairs, query tiles of
     // kPfCols virtual queries, key chunks of kPfKeys keys per group

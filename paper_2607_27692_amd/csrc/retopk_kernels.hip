@@ -529,7 +529,11 @@ __device__ void scan_segment_octet(const StepArgs &a, const Ws &w, int b, int g,
 #pragma unroll
         for (int s = 0; s < NV; ++s) qv[j][s] = qr[s * 8 + o];
     }
-    const bool keep = o < a.G && ((exmask >> o) & 1u);   // head o is exact
+    // head o's scores are stored when it is exact, or (in a scan-fed step) when
+    // it reuses in a scanned group, for its candidates; only exact heads are
+    // counted in the histograms
+    const bool keep = o < a.G && (((exmask >> o) & 1u) || a.scan_fed);
+    const bool count = o < a.G && ((exmask >> o) & 1u);
     uint4 kv[UP][NV];
     int row[UP];                          // rows < len < 2^31
     auto load = [&](int64_t base) {
@@ -560,7 +564,7 @@ __device__ void scan_segment_octet(const StepArgs &a, const Ws &w, int b, int g,
             const float sc = octet_transpose_sum(acc, o) * a.inv_sqrt_d;
             if (keep && row[u] < row1) {
                 w.scores[(int64_t)(bh0 + o) * a.row_stride + row[u]] = sc;
-                atomicAdd(&s_hist[o * kHistBins + (ord_key(sc) >> kHistShift)], 1u);
+                if (count) atomicAdd(&s_hist[o * kHistBins + (ord_key(sc) >> kHistShift)], 1u);
             }
         }
         base += UP * RPP;
@@ -599,7 +603,10 @@ __device__ void scan_segment_mfma(const StepArgs &a, const Ws &w, int b, int g, 
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) qb[ks] = __builtin_bit_cast(bf16x8_t, qr[ks * 4 + kq]);
     }
-    const bool keep = col < a.G && ((exmask >> col) & 1u);   // column col is an exact head
+    // column col's scores are stored when its head is exact, or (in a scan-fed
+    // step) reuses in a scanned group; only exact heads are counted
+    const bool keep = col < a.G && (((exmask >> col) & 1u) || a.scan_fed);
+    const bool count = col < a.G && ((exmask >> col) & 1u);
     float *srow = w.scores + (int64_t)(bh0 + (keep ? col : 0)) * a.row_stride;
     uint32_t *hrow = s_hist + col * kHistBins;
     uint4 kv[TW][KS];
@@ -641,7 +648,7 @@ __device__ void scan_segment_mfma(const StepArgs &a, const Ws &w, int b, int g, 
                 for (int i = 0; i < 4; ++i) {
                     if (r4 + i >= row0 && r4 + i < row1) {
                         if (!whole) srow[r4 + i] = sc[i];
-                        atomicAdd(&hrow[ord_key(sc[i]) >> kHistShift], 1u);
+                        if (count) atomicAdd(&hrow[ord_key(sc[i]) >> kHistShift], 1u);
                     }
                 }
             }
@@ -715,10 +722,13 @@ __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint3
                 for (int jj = 0; jj < (G + 3) / 4; ++jj) {
                     const int j = jj * 4 + (G == 1 ? 0 : (G == 2 ? (p & 1) : p));
                     const bool mine = G == 1 ? p == 0 : (G == 2 ? p < 2 : true);
-                    if (mine && ((exmask >> j) & 1u)) {
+                    // stored for exact heads and (scan-fed steps) for the reuse
+                    // heads of a scanned group; counted for exact heads only
+                    const bool ex = ((exmask >> j) & 1u) != 0u;
+                    if (mine && j < a.G && (ex || a.scan_fed)) {
                         const float sc = (jj == 0 ? sc_lo : sc_hi) * a.inv_sqrt_d;
                         w.scores[(int64_t)(bh0 + j) * a.row_stride + row[u]] = sc;
-                        atomicAdd(&s_hist[j * kHistBins + (ord_key(sc) >> kHistShift)], 1u);
+                        if (ex) atomicAdd(&s_hist[j * kHistBins + (ord_key(sc) >> kHistShift)], 1u);
                     }
                 }
             }
@@ -923,6 +933,22 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
 #pragma unroll
         for (int v = 0; v < R::kNV; ++v) qv[v] = qr[v * 4 + p];
     }
+    // In a scan-fed step: whether the head's KV group is scanned (some head of the
+    // group has every block maximum of rho below tau: it falls back), by the rule
+    // the scan blocks apply; bit j of s_grp: head j of the group reuses.
+    __shared__ uint32_t s_grp;
+    if (a.scan_fed && wave == 0) {
+        const int64_t head0 = (int64_t)b * a.Hq + (int64_t)g * a.G;
+        uint32_t bits = 0u;
+        for (int i = lane; i < a.G * nsb; i += 64) {
+            const int j = i / nsb, sb = i - j * nsb;
+            if (w.rho_bmax[(head0 + j) * (kMaxCache / kSimSlots) + sb] >= (double)a.tau) bits |= 1u << j;
+        }
+        uint32_t all = 0u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) all |= __ballot(((bits >> j) & 1u) != 0u) ? 1u << j : 0u;
+        if (lane == 0) s_grp = all;
+    }
     __syncthreads();
 
     // Eq. 7: merge the blocks' Top-R lists (each sorted best first) in one wave:
@@ -963,8 +989,10 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     for (int i = 0; i < nret_all; ++i) mx = fmax(mx, s_retrho[i]);
     const int8_t path = mx < (double)a.tau ? PATH_FALLBACK : PATH_REUSE;
     const int nret = path == PATH_REUSE ? nret_all : 0;
+    // a reuse head of a scanned group: its candidates' scores come from the scan
+    const bool from_scan = a.scan_fed && path == PATH_REUSE && s_grp != (1u << a.G) - 1u;
     if (s == 0 && tid == 0) {
-        w.path[bh] = path;
+        w.path[bh] = from_scan ? PATH_REUSE_SCANNED : path;
         if (a.dbg_path) a.dbg_path[bh] = path;
         if (a.dbg_rho) a.dbg_rho[bh] = mx;
         atomicAdd(&w.stats[path == PATH_REUSE ? STAT_REUSE : STAT_FALLBACK], 1ull);
@@ -1066,10 +1094,15 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
             }
             __syncthreads();
             const int nr = (int)(seg_total - rb < (uint32_t)kCandList ? seg_total - rb : kCandList);
+            if (from_scan) {
+                // the candidate indices only; k_filter puts in their ranks once the
+                // scan has stored the scores
+                for (int i = tid; i < nr; i += NT) ents[total + rb + i] = (uint64_t)(uint32_t)list[i];
+            }
             // Eq. 10 on this round: 4 lanes per key row, four rows per lane in
             // flight, loaded from clamped (in-bounds) list positions.
             constexpr int GU = 4;
-            for (int base = 0; base < nr; base += GU * kScanRowsPerIter) {
+            for (int base = 0; !from_scan && base < nr; base += GU * kScanRowsPerIter) {
                 uint4 kv[GU][R::kNV];
                 int ci[GU], cidx[GU];
 #pragma unroll
@@ -1104,10 +1137,14 @@ template <typename T, int D, int G, bool kSelect>
 __global__ __launch_bounds__(kScoreThreads, (kGroupWaves<T, D, G>)) void k_score(StepArgs a, Ws w, Geometry geo)
 {
     extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-    if (kSelect && (int)blockIdx.x < geo.cand_blocks)
-        range_block<T, D>(a, w, (int)blockIdx.x, lds);
+    // The host orders the two kinds of block (both counts are multiples of 8, so
+    // a block's XCD does not depend on the order).
+    const int first = kSelect ? (geo.scan_first ? geo.scan_blocks : geo.cand_blocks) : 0;
+    const bool is_range = kSelect && (((int)blockIdx.x < first) != (geo.scan_first != 0));
+    if (is_range)
+        range_block<T, D>(a, w, (int)blockIdx.x - (geo.scan_first ? first : 0), lds);
     else
-        scan_block<T, D, G, kSelect>(a, w, geo, (int)blockIdx.x - (kSelect ? geo.cand_blocks : 0), lds);
+        scan_block<T, D, G, kSelect>(a, w, geo, (int)blockIdx.x - (kSelect && !geo.scan_first ? first : 0), lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -1126,7 +1163,31 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
     const int vh = blockIdx.x / geo.filter_blocks_per_head;   // the head (a.U == 1)
     const int f = blockIdx.x % geo.filter_blocks_per_head;
     const int64_t len = a.U > 1 ? a.len + vh / (a.B * a.Hq) : a.len;
-    if (a.mode == MODE_SELECT && w.path[vh] == PATH_REUSE) return;
+    if (a.mode == MODE_SELECT) {
+        const int8_t path = w.path[vh];
+        if (path == PATH_REUSE) return;
+        if (path == PATH_REUSE_SCANNED) {
+            // Eq. 10 from the scan's scores: the candidate indices of range r
+            // (blocks f, f + fpb, ... of the head) become their ranks
+            for (int r = f; r < kCandRanges; r += geo.filter_blocks_per_head) {
+                uint64_t *ents = w.cand_ent + ((int64_t)vh * kCandRanges + r) * a.cand_cap;
+                const int n = (int)w.cand_cnt[(int64_t)vh * kCandRanges + r];
+                const float *srow = w.scores + (int64_t)vh * a.row_stride;
+                for (int j0 = tid; j0 < n; j0 += 4 * NT) {
+                    uint32_t idx[4];
+                    float sc[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) idx[u] = (uint32_t)ents[j0 + u * NT < n ? j0 + u * NT : j0];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) sc[u] = srow[idx[u]];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        if (j0 + u * NT < n) ents[j0 + u * NT] = rank_of(sc[u], idx[u]);
+                }
+            }
+            return;
+        }
+    }
 
     // This block's scores and the head's histogram in one round trip.
     const int64_t i0 = (int64_t)f * kFilterRows + (int64_t)tid * EPT;
@@ -1476,7 +1537,7 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
         }
         const uint32_t rc = reuse ? cnt_r : cnt_x;
         const bool fits = spec > 0 && __ballot(lane < nreg && rc > (uint32_t)spec) == 0ull;
-        if (sel_mode && path != PATH_REUSE) {
+        if (sel_mode && path != PATH_REUSE && path != PATH_REUSE_SCANNED) {
             reuse = false;
             base = w.surv + (int64_t)bh * a.row_stride;
             stride = kFilterRows;
@@ -1839,7 +1900,8 @@ __global__ __launch_bounds__(kFinalThreads) void k_final(StepArgs a, Ws w)
     // region in one round trip (the entry loads are speculative: a region's
     // count is known only afterwards).
     const bool sel_mode = a.mode == MODE_SELECT;
-    const bool reuse = sel_mode && w.path[bh] == PATH_REUSE;
+    const int8_t path_g = sel_mode ? w.path[bh] : (int8_t)PATH_FALLBACK;
+    const bool reuse = path_g == PATH_REUSE || path_g == PATH_REUSE_SCANNED;
     const int nreg_s = (int)((len + kFilterRows - 1) / kFilterRows);
     const int rpt = (nreg_s + NT - 1) / NT;
     uint32_t scnt[kRegPerThread];
