@@ -969,6 +969,7 @@ SYMBOLS = {  # kernel symbol prefix -> name used by the library's own profiling
     "void retopk::k_dense<": "dense_chunk",
     "void retopk::k_dense_merge<": "dense_merge",
     "void retopk::k_pf_score<": "prefill_score",
+    "void retopk::k_scan_list<": "retopk_scan",
 }
 
 

@@ -127,6 +127,12 @@ Geometry step_geometry(const retopk_config &c, int64_t len, int mode)
     // carry the step's critical path, go first.
     g.scan_first = g.cand_blocks > kCUs;
     g.filter_blocks_per_head = (int)ceil_div(len, kFilterRows);
+    // Every group scanned, groups of at most 4 heads (the quad row layout) and
+    // at least one whole filter region per CU: one k_scan_list block per whole
+    // region keeps the region's scores in LDS and writes its local survivors only.
+    g.list_mode = (mode == MODE_EXACT || mode == MODE_REFRESH || mode == MODE_COLD) &&
+                  c.n_q_heads / c.n_kv_heads <= 4 &&
+                  (int64_t)c.batch * c.n_kv_heads * (len / kFilterRows) >= kCUs;
     return g;
 }
 

@@ -131,6 +131,8 @@ struct Geometry {
     int cand_blocks;           // ceil(B * Hq / 8) * 8 * kCandRanges in MODE_SELECT, else 0
     int scan_first;            // k_score's scan blocks come before its range blocks
     int filter_blocks_per_head;
+    int list_mode;             // every KV group scanned by k_scan_list, one block per
+                               // filter region: k_filter reads local survivors
     // batched prefill (k_pf_score): (KV group, key chunk) pairs, query tiles of
     // kPfCols virtual queries, key chunks of kPfKeys keys per group
     int pf_pairs, pf_qtiles, pf_kchunks;

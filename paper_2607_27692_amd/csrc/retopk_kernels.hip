@@ -1189,10 +1189,29 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
         }
     }
 
-    // This block's scores and the head's histogram in one round trip.
+    // This block's scores (or, after k_scan_list, the region's count and its
+    // first 2 * NT local survivors) and the head's histogram in one round trip.
     const int64_t i0 = (int64_t)f * kFilterRows + (int64_t)tid * EPT;
-    const float4 *src = (const float4 *)(w.scores + (int64_t)vh * a.row_stride + i0);
-    const float4 v0 = src[0], v1 = src[1];
+    uint64_t *reg = w.surv + (int64_t)vh * a.row_stride + (int64_t)f * kFilterRows;
+    float4 v0, v1;
+    uint4 lv, lv2 = {};
+    uint32_t nloc = 0u;
+    // after k_scan_list, a whole region holds its local survivors; the rows past
+    // the last whole region are in the score row
+    const bool listed = geo.list_mode && f < (int)(len / kFilterRows);
+    if (listed) {
+        nloc = w.surv_cnt[(int64_t)vh * a.n_regions + f];
+        if (a.K > 512) {
+            lv = ((const uint4 *)reg)[2 * tid];
+            lv2 = ((const uint4 *)reg)[2 * tid + 1];
+        } else {
+            lv = ((const uint4 *)reg)[tid];
+        }
+    } else {
+        const float4 *src = (const float4 *)(w.scores + (int64_t)vh * a.row_stride + i0);
+        v0 = src[0];
+        v1 = src[1];
+    }
     const uint32_t *hist = w.hist + (int64_t)vh * kHistBins;
     uint32_t c[4];
 #pragma unroll
@@ -1212,6 +1231,42 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
         __syncthreads();
     }
     const uint32_t kmin = s_bstar << kHistShift;
+    if (listed) {
+        // The region's local survivors at or above b*, compacted in place in
+        // index order: thread t holds entries m t .. m t + m-1, with m = 2 (4 for
+        // K > 512) from the first round trip, or m = 8 when the region kept more,
+        // all read before the scan's barriers.
+        uint64_t e[EPT] = {};
+        int m = a.K > 512 ? 4 : 2;
+        if (nloc <= (uint32_t)(m * NT)) {
+            e[0] = ((uint64_t)lv.y << 32) | lv.x;
+            e[1] = ((uint64_t)lv.w << 32) | lv.z;
+            e[2] = ((uint64_t)lv2.y << 32) | lv2.x;
+            e[3] = ((uint64_t)lv2.w << 32) | lv2.z;
+        } else {
+            m = EPT;
+#pragma unroll
+            for (int u = 0; u < EPT / 2; ++u) {
+                const uint4 x = ((const uint4 *)reg)[EPT / 2 * tid + u];
+                e[2 * u] = ((uint64_t)x.y << 32) | x.x;
+                e[2 * u + 1] = ((uint64_t)x.w << 32) | x.z;
+            }
+        }
+        uint32_t keep = 0, n = 0;
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            const bool k = u < m && (uint32_t)(m * tid + u) < nloc && rank_key(e[u]) >= kmin;
+            keep |= (uint32_t)k << u;
+            n += k ? 1u : 0u;
+        }
+        uint32_t total;
+        uint32_t pos = block_excl_scan<NT>(n, s_red, &total);
+#pragma unroll
+        for (int u = 0; u < EPT; ++u)
+            if ((keep >> u) & 1u) reg[pos++] = e[u];
+        if (tid == 0) w.surv_cnt[(int64_t)vh * a.n_regions + f] = total;
+        return;
+    }
     const float sv[EPT] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
     uint32_t keep = 0, n = 0;
 #pragma unroll
@@ -2603,6 +2658,249 @@ __global__ __launch_bounds__(kMergeThreads) void k_dense_merge(StepArgs a, Ws w)
 }
 
 // ---------------------------------------------------------------------------
+// k_scan_list: the full-history scan of every KV group (exact, refresh and cold
+// steps) when the groups' whole filter regions of kFilterRows rows give every
+// CU at least one.  One block per whole region keeps the region's scores in
+// LDS and writes only the entries in the bins at or above the one holding the
+// region's own K-th largest score, as ranks in index order (the region's local
+// survivors), with their count in surv_cnt.  The rows past the last whole
+// region of a group are shared out over the group's blocks, which write those
+// scores to the score row as the score-row scan does.  k_filter then keeps the
+// entries at or above the head's threshold bin b* (Eq. 1 through the
+// histogram): a block's rows are a subset of the head's, so at least K of the
+// head's rows lie in bins at or above the block's local bin, b* is never below
+// it, and the global survivors are exactly those the score-row path compacts.
+// For the same reason a block adds to the head's histogram only its counts of
+// the bins from its local bin up: the counts k_filter sums from the top down to
+// b* are complete, and it reads no lower bin.
+// One block per CU (its LDS holds the region's scores and histograms): 1024
+// threads where the group's query vectors and two key rows a lane fit in 128
+// registers, else 512 threads with up to 256; each lane keeps the next pass's
+// key rows in flight while it scores the current ones.
+// ---------------------------------------------------------------------------
+
+__host__ __device__ constexpr int scan_list_lds(int g) { return g * (kFilterRows + kHistBins) * 4; }
+
+template <typename T, int D, int G>
+constexpr int kListThreads = (G + 2) * RowT<T, D>::kNV * 4 <= 96 ? 1024 : 512;
+template <typename T, int D, int G>
+constexpr int kListRowsInFlight = kListThreads<T, D, G> == 1024 ? 1 : ((G + 4) * RowT<T, D>::kNV * 4 <= 192 ? 2 : 1);
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__((kListThreads<T, D, G>), (kListThreads<T, D, G> / 256)) void k_scan_list(StepArgs a, Ws w)
+{
+    using R = RowT<T, D>;
+    constexpr int NT = kListThreads<T, D, G>, NW = NT / 64;
+    constexpr int U = kListRowsInFlight<T, D, G>;       // rows per lane per pass
+    constexpr int RPP = NT / 4;                          // rows per pass and row slot
+    constexpr int STEP = U * RPP;                        // rows per pass
+    constexpr int WPH = NW / G;                          // compaction waves per head
+    constexpr int RPL = kFilterRows / (WPH * 64);        // compaction rows per lane
+    static_assert(G == 1 || G == 2 || G == 4, "quad row layout");
+    static_assert(kFilterRows % (2 * STEP) == 0 && RPL % 4 == 0 && RPL <= 32, "region geometry");
+    extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+    float *s_sc = (float *)lds;                                       // [G][kFilterRows]
+    uint32_t *s_hist = (uint32_t *)(lds + G * kFilterRows * 4);       // [G][kHistBins]
+    __shared__ uint32_t s_bloc[G];
+    __shared__ uint32_t s_wcnt[NW];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3, rl = lane >> 2;
+    const int nfull = (int)(a.len / kFilterRows);        // whole regions per group (>= 1)
+    const int gi = (int)blockIdx.x / nfull, f = (int)blockIdx.x - gi * nfull;
+    const int b = gi / a.Hkv, g = gi % a.Hkv;
+    const int bh0 = b * a.Hq + g * a.G;
+    const int64_t r0 = (int64_t)f * kFilterRows;
+    const T *gbase = (const T *)a.k + ((int64_t)b * a.Hkv + g) * a.max_len * D;
+    const T *kbase = gbase + r0 * D;
+    // this block's share of the rows past the last whole region: [x0, x1)
+    const int64_t tail0 = (int64_t)nfull * kFilterRows;
+    const int64_t xs = ((a.len - tail0) + nfull - 1) / nfull;
+    const int64_t x0 = tail0 + f * xs < a.len ? tail0 + f * xs : a.len;
+    const int64_t x1 = x0 + xs < a.len ? x0 + xs : a.len;
+
+    uint4 qv[G][R::kNV];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+        const int hj = j < a.G ? j : 0;   // heads past a.G pad the group
+        const uint4 *qr = (const uint4 *)((const T *)a.q + (int64_t)(bh0 + hj) * a.q_head_stride);
+#pragma unroll
+        for (int v = 0; v < R::kNV; ++v) qv[j][v] = qr[v * 4 + p];
+    }
+    // Key rows base + u * RPP + wave * 16 + rl of a pass, from clamped (in-bounds)
+    // rows; two register sets, so that a pass's loads are issued before the
+    // previous pass is scored.
+    uint4 kA[U][R::kNV], kB[U][R::kNV];
+    auto load = [&](uint4 (&kv)[U][R::kNV], const T *src, int base, int n) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int r = base + u * RPP + wave * 16 + rl;
+            const uint4 *rp = (const uint4 *)(src + (int64_t)(r < n ? r : 0) * D);
+#pragma unroll
+            for (int v = 0; v < R::kNV; ++v) kv[u][v] = rp[v * 4 + p];
+        }
+    };
+    // Scores of a pass: to LDS (the region) or to the score row (rows past the
+    // last whole region), counted in the block's histograms either way.
+    auto score = [&](const uint4 (&kv)[U][R::kNV], int base, int n, float *row_out) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int r = base + u * RPP + wave * 16 + rl;
+            float acc[G];
+#pragma unroll
+            for (int j = 0; j < G; ++j) {
+                float s0 = 0.0f;
+#pragma unroll
+                for (int v = 0; v < R::kNV; ++v) s0 = Dot<T>::f(kv[u][v], qv[j][v], s0);
+                acc[j] = s0;
+            }
+            float sc_lo, sc_hi;
+            group_scores<G>(acc, p, sc_lo, sc_hi);
+            const int j = G == 1 ? 0 : (G == 2 ? (p & 1) : p);
+            const bool mine = G == 1 ? p == 0 : (G == 2 ? p < 2 : true);
+            if (mine && j < a.G && r < n) {
+                const float sc = sc_lo * a.inv_sqrt_d;
+                if (row_out) row_out[(int64_t)j * a.row_stride + r] = sc;
+                else s_sc[j * kFilterRows + r] = sc;
+                atomicAdd(&s_hist[j * kHistBins + (ord_key(sc) >> kHistShift)], 1u);
+            }
+        }
+    };
+    load(kA, kbase, 0, kFilterRows);   // the first rows are in flight while the histogram is cleared
+    for (int i = tid; i < G * kHistBins; i += NT) s_hist[i] = 0u;
+    __syncthreads();
+    for (int base = 0; base < kFilterRows; base += 2 * STEP) {
+        load(kB, kbase, base + STEP, kFilterRows);
+        score(kA, base, kFilterRows, nullptr);
+        if (base + 2 * STEP < kFilterRows) load(kA, kbase, base + 2 * STEP, kFilterRows);
+        score(kB, base + STEP, kFilterRows, nullptr);
+    }
+    if (x1 > x0) {
+        const int nx = (int)(x1 - x0);
+        float *row_out = w.scores + (int64_t)bh0 * a.row_stride + x0;
+        for (int base = 0; base < nx; base += STEP) {
+            load(kA, gbase + x0 * D, base, nx);
+            score(kA, base, nx, row_out);
+        }
+    }
+    __syncthreads();
+
+    // Wave j: the bin holding head j's K-th largest score of the block.  Lane l
+    // reads the 4-bin groups l + 64 i (i = 0..7: chunk i holds bins 256 i ..
+    // 256 i + 255), so that the wave's reads are contiguous; the chunk totals
+    // locate the chunk, a suffix sum over the lanes the group, the lane the bin.
+    // The lanes keep their counts for the histogram flush at the end (no barrier
+    // then waits for those atomics).
+    uint32_t c[8][4];
+    uint32_t bloc = 0u;
+    if (wave < a.G) {
+        const uint4 *hv = (const uint4 *)(s_hist + wave * kHistBins);
+        uint32_t cs[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint4 x = hv[i * 64 + lane];
+            c[i][0] = x.x;
+            c[i][1] = x.y;
+            c[i][2] = x.z;
+            c[i][3] = x.w;
+            cs[i] = x.x + x.y + x.z + x.w;
+        }
+        const uint32_t kn = (uint32_t)a.K;              // <= kFilterRows rows counted
+        uint32_t above = 0u, ic = 0u;
+        bool found = false;
+#pragma unroll
+        for (int i = 7; i >= 0; --i) {
+            const uint32_t t = wave_incl_scan(cs[i]);
+            const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)t, 63);
+            if (!found && above + tot >= kn) {
+                found = true;
+                ic = (uint32_t)i;
+            } else if (!found) {
+                above += tot;
+            }
+        }
+        // chunk ic: lane l's group holds bins 4 (l + 64 ic) .. + 3; the count in
+        // higher lanes of the chunk is tot - inclusive prefix
+        uint32_t my[4], mys = 0u;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            if ((uint32_t)i == ic) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) my[e] = c[i][e];
+                mys = cs[i];
+            }
+        const uint32_t inc = wave_incl_scan(mys);
+        const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+        const uint32_t hi = above + tot - inc;           // count in bins above this lane's
+        const uint64_t hit = __ballot(hi < kn && hi + mys >= kn);
+        const int src = __builtin_ctzll(hit);
+        uint32_t bs = 0u, run = hi;
+#pragma unroll
+        for (int e = 3; e >= 0; --e) {
+            if (run < kn && run + my[e] >= kn) bs = 4u * ((uint32_t)lane + 64u * ic) + (uint32_t)e;
+            run += my[e];
+        }
+        bloc = (uint32_t)__builtin_amdgcn_readlane((int)bs, src);
+        if (lane == 0) s_bloc[wave] = bloc;
+    }
+    __syncthreads();
+
+    // Local survivors in index order: WPH waves per head; wave k of head j holds
+    // rows k * 64 * RPL .. of the region in RPL / 4 chunks of 256 rows, lane l
+    // rows 4 l .. 4 l + 3 of each chunk (contiguous LDS reads), ranked chunk by
+    // chunk with wave prefix sums.
+    {
+        constexpr int NC = RPL / 4;
+        const int j = wave / WPH, k = wave - j * WPH;
+        const int w0 = k * 64 * RPL;
+        float sv[NC][4];
+        uint32_t cnt[NC], pre[NC], wtot = 0u;
+#pragma unroll
+        for (int ch = 0; ch < NC; ++ch) {
+            cnt[ch] = 0u;
+            if (j < a.G) {
+                const float4 x = *(const float4 *)&s_sc[j * kFilterRows + w0 + ch * 256 + 4 * lane];
+                sv[ch][0] = x.x;
+                sv[ch][1] = x.y;
+                sv[ch][2] = x.z;
+                sv[ch][3] = x.w;
+                const uint32_t kmin = s_bloc[j] << kHistShift;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) cnt[ch] += ord_key(sv[ch][e]) >= kmin ? 1u : 0u;
+            }
+            const uint32_t inc = wave_incl_scan(cnt[ch]);
+            pre[ch] = wtot + inc - cnt[ch];
+            wtot += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+        }
+        if (lane == 0) s_wcnt[wave] = wtot;
+        __syncthreads();
+        if (j < a.G) {
+            uint32_t off = 0u;
+            for (int k2 = 0; k2 < k; ++k2) off += s_wcnt[j * WPH + k2];
+            const uint32_t kmin = s_bloc[j] << kHistShift;
+            uint64_t *dst = w.surv + (int64_t)(bh0 + j) * a.row_stride + r0;
+#pragma unroll
+            for (int ch = 0; ch < NC; ++ch) {
+                uint32_t at = off + pre[ch];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (ord_key(sv[ch][e]) >= kmin)
+                        dst[at++] = rank_of(sv[ch][e], (uint32_t)(r0 + w0 + ch * 256 + 4 * lane + e));
+            }
+            if (k == WPH - 1 && lane == 0) w.surv_cnt[(int64_t)(bh0 + j) * a.n_regions + f] = off + wtot;
+        }
+    }
+    if (wave < a.G) {
+        uint32_t *gh = w.hist + (int64_t)(bh0 + wave) * kHistBins;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t bin = 4u * ((uint32_t)lane + 64u * (uint32_t)i) + (uint32_t)e;
+                if (c[i][e] && bin >= bloc) atomicAdd(&gh[bin], c[i][e]);
+            }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
 
@@ -2623,6 +2921,14 @@ static void sim_desc(const StepArgs &a, KernelDesc *k)
 template <typename T, int D, int G>
 static void score_desc(const StepArgs &a, const Geometry &geo, KernelDesc *k)
 {
+    if constexpr (G <= 4) {
+        if (geo.list_mode) {
+            const unsigned blocks = (unsigned)((int64_t)a.B * a.Hkv * (a.len / kFilterRows));
+            *k = KernelDesc{(const void *)&k_scan_list<T, D, G>, dim3(blocks),
+                            dim3((unsigned)kListThreads<T, D, G>), (unsigned)scan_list_lds(G), 2};
+            return;
+        }
+    }
     const unsigned blocks = (unsigned)(geo.scan_blocks + geo.cand_blocks);
     if (a.mode == MODE_SELECT) {
         const int n_merge = ((a.M + kSimSlots - 1) / kSimSlots) * a.R;

@@ -58,6 +58,14 @@ CASES = [
     ("bf16", 64, 2, 6, 2, 5000, 96, "randn"),      # 3
     ("f32", 128, 1, 10, 2, 3000, 64, "randn"),     # 5
     ("bf16", 128, 1, 12, 2, 4500, 200, "ties"),    # 6
+    # at least one 4096-row filter region per CU (B * Hkv * regions >= 256): every
+    # region scanned by one block that keeps its scores in LDS and writes only its
+    # local survivors; the shorter second length runs the score-row scan
+    ("bf16", 128, 2, 128, 32, 20000, 512, "randn"),
+    ("bf16", 128, 1, 64, 64, 16500, 2048, "ties"),     # > 1024 local survivors a region
+    ("f32", 128, 1, 192, 64, 13000, 300, "randn"),     # 3 heads a group; 2 rows a lane
+    ("bf16", 64, 4, 32, 16, 16385, 77, "negative"),
+    ("f32", 64, 1, 64, 64, 12289, 40, "equal"),        # every row of a region survives
 ]
 
 
