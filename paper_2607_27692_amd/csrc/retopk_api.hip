@@ -105,6 +105,27 @@ StepArgs config_args(const retopk_config &c)
     return a;
 }
 
+// The range blocks' index ranges of a decode step that selects (Eq. 8-9 split
+// over kCandRanges blocks per head).  Every row of the window [w0, len) is a
+// candidate, so the window gets ranges of its own, about as many as its share
+// of the candidates (W rows against R * K support entries, weighted 10 : 3),
+// so that no range block gathers far more rows than the others; the ranges
+// stay in index order.
+void range_split(StepArgs &a)
+{
+    a.w0 = a.len - a.W > 0 ? a.len - a.W : 0;
+    a.n_win = 0;
+    if (a.W > 0) {
+        const int64_t share = (10ll * kCandRanges * a.W + 10ll * a.W + 3ll * a.R * a.K - 1) /
+                              (10ll * a.W + 3ll * a.R * a.K);
+        a.n_win = a.w0 == 0 ? kCandRanges
+                            : (int)(share < 1 ? 1 : (share > kCandRanges - 1 ? kCandRanges - 1 : share));
+    }
+    const int n_old = kCandRanges - a.n_win;
+    a.span_old = n_old > 0 ? (a.w0 + n_old - 1) / n_old : 0;
+    a.span_win = a.n_win > 0 ? (a.len - a.w0 + a.n_win - 1) / a.n_win : 0;
+}
+
 Geometry step_geometry(const retopk_config &c, int64_t len, int mode)
 {
     Geometry g{};
@@ -449,6 +470,7 @@ retopk_status retopk_decode_step(retopk_handle h, const void *q, const void *k, 
     a.k = k;
     a.v = v;
     a.len = len;
+    if (mode == MODE_SELECT) range_split(a);
     a.out = out;
     a.sel = sel;
     a.n_ins = h->n_ins;

@@ -108,6 +108,11 @@ struct StepArgs {
     const void *k;
     const void *v;
     int64_t len;               // with U > 1: the length of position 0 of the launch
+    // MODE_SELECT: the split of [0, len) into the range blocks' index ranges
+    // (range_split): ranges 0 .. kCandRanges-n_win-1 cover [0, w0) in spans of
+    // span_old rows, the others the window [w0, len) in spans of span_win
+    int64_t w0, span_old, span_win;
+    int n_win;
     int U;                     // query positions per launch: 1, or more in the batched
                                // prefill, where virtual head vh = u * B * Hq + bh holds
                                // position u (length len + u, q at + u * d, slot
@@ -165,6 +170,7 @@ inline int64_t heads_of(const retopk_config &c) { return (int64_t)c.batch * c.n_
 // step-dependent field left zero), and the launch geometry of a step.
 retopk_status validate_config(const retopk_config *c);
 StepArgs config_args(const retopk_config &c);
+void range_split(StepArgs &a);
 Geometry step_geometry(const retopk_config &c, int64_t len, int mode);
 
 // Fills *k for kernel `which` of a step in a.mode (retopk_kernels.hip).

@@ -365,11 +365,6 @@ __device__ void block_qbar(const T *q, float *s_qbar, double *red)
 // k_sim: rho for 64 cache slots per block (Eq. 6)
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ bool better(double ra, int aa, double rb, int ab)
-{
-    return ra > rb || (ra == rb && aa < ab);
-}
-
 // Age of a cache slot: 0 for the most recent insertion, (n_ins - 1 - slot) mod C.
 __device__ __forceinline__ int slot_age(int age0, int slot, int M)
 {
@@ -383,8 +378,8 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
     constexpr int NT = kSimThreads;
     __shared__ float s_qbar[D];
     __shared__ double s_red[NT / 64];
-    __shared__ double s_rho[kSimSlots];
-    __shared__ int s_age[kSimSlots];
+    __shared__ __attribute__((aligned(16))) double s_rho[kSimSlots];
+    __shared__ __attribute__((aligned(16))) int s_age[kSimSlots];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, p = lane & 3;
     const int M = a.M;
     const int nsb = (M + kSimSlots - 1) / kSimSlots;
@@ -419,7 +414,7 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
         acc += (double)c[s].w * (double)qq[3];
     }
     acc = quad_sum(acc);
-    const int age0 = (int)((a.n_ins - 1) % M);
+    const int age0 = a.insert_slot > 0 ? a.insert_slot - 1 : M - 1;   // slot of the newest entry
     if (p == 0) {
         s_rho[local] = slot < n_valid ? acc : -INFINITY;
         s_age[local] = slot < n_valid ? slot_age(age0, slot, M) : 0x7FFFFFFF;
@@ -437,11 +432,32 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
     {
         const double ri = s_rho[local];
         const int ai = s_age[local];
-        int cnt = 0;
+        // the 16 slots this lane compares against, read (16-byte reads) before
+        // any comparison, then counted without branches
+        double ro[16];
+        int ao[16];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const int o = p * 16 + u;
-            cnt += (recent ? s_age[o] < ai : better(s_rho[o], s_age[o], ri, ai)) ? 1 : 0;
+        for (int u = 0; u < 8; ++u) {
+            const double2 x = ((const double2 *)&s_rho[p * 16])[u];
+            ro[2 * u] = x.x;
+            ro[2 * u + 1] = x.y;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int4 x = ((const int4 *)&s_age[p * 16])[u];
+            ao[4 * u] = x.x;
+            ao[4 * u + 1] = x.y;
+            ao[4 * u + 2] = x.z;
+            ao[4 * u + 3] = x.w;
+        }
+        int cnt = 0;
+        if (recent) {
+#pragma unroll
+            for (int u = 0; u < 16; ++u) cnt += ao[u] < ai ? 1 : 0;
+        } else {
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                cnt += ((ro[u] > ri) | ((ro[u] == ri) & (ao[u] < ai))) ? 1 : 0;
         }
         cnt += __builtin_amdgcn_mov_dpp(cnt, kQuadXor1, 0xF, 0xF, true);
         cnt += __builtin_amdgcn_mov_dpp(cnt, kQuadXor2, 0xF, 0xF, true);
@@ -878,7 +894,7 @@ template <typename T, int D>
 __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned char *lds)
 {
     using R = RowT<T, D>;
-    constexpr int NT = kScoreThreads;
+    constexpr int NT = kScoreThreads, NW = NT / 64;
     const int kCands = ((a.M + kSimSlots - 1) / kSimSlots) * a.R;   // merge candidates
     __shared__ uint32_t s_red32[NT / 64];
     __shared__ int32_t s_ret[kMaxR];
@@ -899,6 +915,7 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     int32_t *c_slot = (int32_t *)(lds + 8 * kCands);
     int32_t *c_cnt = (int32_t *)(lds + 12 * kCands);
     int32_t *c_age = (int32_t *)(lds + 16 * kCands);
+    int32_t *c_rank = (int32_t *)(lds + 20 * kCands);
     const int b = bh / a.Hq, h = bh % a.Hq, g = h / a.G;
 
     // Retrieved positions no list entry fills stay empty (possible only when the
@@ -912,7 +929,7 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     // most similar first, invalid entries last) and q.
     const int per = a.R;                        // list length of a full k_sim block
     const int nc = nsb * per;
-    const int age0 = (int)((a.n_ins - 1) % M);
+    const int age0 = a.insert_slot > 0 ? a.insert_slot - 1 : M - 1;   // slot of the newest entry
     for (int c = tid; c < nc; c += NT) {
         const int sb = c / per, j = c - sb * per;
         const int nloc = n_valid - sb * kSimSlots;
@@ -926,6 +943,7 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
         c_rho[c] = use ? rr : -INFINITY;
         c_cnt[c] = use ? cn : 0;
         c_age[c] = use ? slot_age(age0, sl, M) : 0x7FFFFFFF;
+        c_rank[c] = 0;
     }
     uint4 qv[R::kNV];
     {
@@ -951,34 +969,43 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     }
     __syncthreads();
 
-    // Eq. 7: merge the blocks' Top-R lists (each sorted best first) in one wave:
-    // lane o holds the head of list o, and each round the best head (the most
-    // similar, then the newer; for recent-R retrieval the newer) is retrieved and
-    // its list advances.  Heads that compare with nothing (non-finite similarity)
-    // are never taken, and the round ends the merge when no head is left.
-    if (wave == 0) {
+    // Eq. 7 over the k_sim blocks' lists (their union holds the global Top-R):
+    // a listed candidate's rank is the number of listed candidates before it --
+    // more similar, or equally similar and newer (for recent-R retrieval: newer)
+    // -- and ranks 0 .. nret_all-1 are retrieved.  Ages are distinct, so the ranks
+    // are; a candidate whose similarity is not ordered (NaN) is never taken.
+    // Each wave counts one share of the comparisons; LDS adds the shares.
+    {
         const bool recent = a.retrieval == 1;
-        int ptr = 0;
-        for (int k = 0; k < nret_all; ++k) {
-            const int e = lane * per + (ptr < per ? ptr : per - 1);
-            const bool live = lane < nsb && ptr < per && c_slot[e] >= 0;
-            const double rh = live ? c_rho[e] : -INFINITY;
-            const uint32_t ah = live ? (uint32_t)c_age[e] : 0xFFFFFFFFu;
-            bool cand = live;
-            if (!recent) {
-                const double m = wave_max_f64(rh);
-                cand = live && rh == m;
+        const int jper = (nc + NW - 1) / NW;
+        const int j0 = wave * jper, j1 = j0 + jper < nc ? j0 + jper : nc;
+        for (int c = lane; c < nc; c += 64) {
+            const double rc = c_rho[c];
+            const int ac = c_age[c];
+            int part = 0;
+            if (recent) {
+                for (int j = j0; j < j1; ++j) part += ((c_slot[j] >= 0) & (c_age[j] < ac)) ? 1 : 0;
+            } else {
+#pragma unroll 4
+                for (int j = j0; j < j1; ++j) {
+                    const double rj = c_rho[j];
+                    const int aj = c_age[j];
+                    const bool ej = (c_slot[j] >= 0) & (rj == rj);
+                    part += (ej & ((rj > rc) | ((rj == rc) & (aj < ac)))) ? 1 : 0;
+                }
             }
-            const uint32_t amin = ~wave_max_u32(cand ? ~ah : 0u);
-            const uint64_t win = __ballot(cand && ah == amin);
-            if (win == 0ull) break;
-            const int wl = __builtin_ctzll(win);
-            if (lane == wl) {
-                s_ret[k] = c_slot[e];
-                s_retcnt[k] = c_cnt[e];
-                s_retrho[k] = rh;
-                ++ptr;
-            }
+            if (part) atomicAdd(&c_rank[c], part);
+        }
+    }
+    __syncthreads();
+    for (int c = tid; c < nc; c += NT) {
+        const int rk = c_rank[c];
+        const int32_t sl = c_slot[c];
+        const double rc = c_rho[c];
+        if (sl >= 0 && rc == rc && rk < nret_all) {
+            s_ret[rk] = sl;
+            s_retcnt[rk] = c_cnt[c];
+            s_retrho[rk] = rc;
         }
     }
     __syncthreads();
@@ -1005,27 +1032,18 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
     if (s == 0 && a.dbg_ret)
         for (int i = tid; i < a.R; i += NT) a.dbg_ret[(int64_t)bh * a.R + i] = i < nret ? s_ret[i] : -1;
 
-    // Eq. 8-9 restricted to this block's index range [lo, hi).  The window (every
-    // one of its rows is a candidate) gets ranges of its own, about as many as its
-    // share of the candidates, so that no range block gathers far more rows than
-    // the others; the ranges stay in index order.
+    // Eq. 8-9 restricted to this block's index range [lo, hi) of the split the
+    // host made for the step (the window's rows in ranges of their own).
     const int64_t len = a.len;
-    const int64_t w0 = len - a.W > 0 ? len - a.W : 0;
-    int n_win = 0;                                   // ranges covering [w0, len)
-    if (a.W > 0) {
-        const int64_t share = (10ll * kCandRanges * a.W + 10ll * a.W + 3ll * a.R * a.K - 1) / (10ll * a.W + 3ll * a.R * a.K);
-        n_win = w0 == 0 ? kCandRanges : (int)(share < 1 ? 1 : (share > kCandRanges - 1 ? kCandRanges - 1 : share));
-    }
-    const int n_old = kCandRanges - n_win;           // ranges covering [0, w0)
+    const int64_t w0 = a.w0;
+    const int n_old = kCandRanges - a.n_win;         // ranges covering [0, w0)
     int64_t lo, hi;
     if (s < n_old) {
-        const int64_t span = (w0 + n_old - 1) / n_old;
-        lo = (int64_t)s * span;
-        hi = lo + span < w0 ? lo + span : w0;
+        lo = (int64_t)s * a.span_old;
+        hi = lo + a.span_old < w0 ? lo + a.span_old : w0;
     } else {
-        const int64_t span = (len - w0 + n_win - 1) / n_win;
-        lo = w0 + (int64_t)(s - n_old) * span;
-        hi = lo + span < len ? lo + span : len;
+        lo = w0 + (int64_t)(s - n_old) * a.span_win;
+        hi = lo + a.span_win < len ? lo + a.span_win : len;
     }
     if (lo > hi) lo = hi;
     uint32_t *bitmap = (uint32_t *)lds;                    // reuses the merge space
