@@ -71,7 +71,6 @@ struct Ws {
     int32_t *supp;        // [BH, C, K], ascending, -1 padded
     int32_t *cnt;         // [BH, C]
     // per-step workspaces
-    double *rho;          // [BH, C] cosine similarities of this step
     double *rho_bmax;     // [BH, kMaxCache / kSimSlots] per-k_sim-block maxima of rho
     int32_t *topr;        // [BH, kMaxCache / kSimSlots, kMaxR] per-k_sim-block Top-R slots
     double *topr_rho;     // [BH, kMaxCache / kSimSlots, kMaxR] their similarities

@@ -418,7 +418,6 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
     if (p == 0) {
         s_rho[local] = slot < n_valid ? acc : -INFINITY;
         s_age[local] = slot < n_valid ? slot_age(age0, slot, M) : 0x7FFFFFFF;
-        if (slot < n_valid) w.rho[(int64_t)bh * M + slot] = acc;
     }
     __syncthreads();
 
@@ -1178,8 +1177,13 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
     __shared__ uint32_t s_red[NT / 64];
     __shared__ uint32_t s_bstar;
     const int tid = threadIdx.x;
-    const int vh = blockIdx.x / geo.filter_blocks_per_head;   // the head (a.U == 1)
-    const int f = blockIdx.x % geo.filter_blocks_per_head;
+    // the filter blocks of (virtual) head vh run on XCD vh % 8 (block j is placed
+    // on XCD j % 8), where the head's range blocks wrote its path and candidates
+    // and its final blocks read the survivors
+    const int x8 = (int)blockIdx.x & 7, rest = (int)blockIdx.x >> 3;
+    const int f = rest % geo.filter_blocks_per_head;
+    const int vh = (rest / geo.filter_blocks_per_head) * 8 + x8;
+    if (vh >= a.B * a.Hq * a.U) return;
     const int64_t len = a.U > 1 ? a.len + vh / (a.B * a.Hq) : a.len;
     if (a.mode == MODE_SELECT) {
         const int8_t path = w.path[vh];
@@ -3024,8 +3028,9 @@ void describe_kernel(int which, int dtype, const StepArgs &a, const Geometry &ge
         if (bf) return d64 ? score_g<uint16_t, 64>(a, geo, k) : score_g<uint16_t, 128>(a, geo, k);
         return d64 ? score_g<float, 64>(a, geo, k) : score_g<float, 128>(a, geo, k);
     case KERNEL_FILTER:
+        // whole groups of 8 (virtual) heads, one per XCD
         *k = KernelDesc{(const void *)&k_filter,
-                        dim3((unsigned)(a.B * a.Hq * a.U * geo.filter_blocks_per_head)),
+                        dim3((unsigned)((a.B * a.Hq * a.U + 7) / 8 * 8 * geo.filter_blocks_per_head)),
                         dim3(kScoreThreads), 0u, 3};
         return;
     case KERNEL_PF_SCORE:   // bf16 only
