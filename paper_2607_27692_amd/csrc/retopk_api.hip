@@ -408,7 +408,7 @@ retopk_status retopk_create(const retopk_config *cfg, retopk_handle *out)
     if ((st = alloc(h, &w.qbar, (size_t)(BH * C * D))) != RETOPK_OK ||
         (st = alloc(h, &w.supp, (size_t)(BH * C * K))) != RETOPK_OK ||
         (st = alloc(h, &w.cnt, (size_t)(BH * C))) != RETOPK_OK ||
-        (st = alloc(h, &w.rho_bmax, (size_t)(BH * NSB))) != RETOPK_OK ||
+        (st = alloc(h, &w.reuse, (size_t)BH)) != RETOPK_OK ||
         (st = alloc(h, &w.topr, (size_t)(BH * NSB * kMaxR))) != RETOPK_OK ||
         (st = alloc(h, &w.topr_rho, (size_t)(BH * NSB * kMaxR))) != RETOPK_OK ||
         (st = alloc(h, &w.topr_cnt, (size_t)(BH * NSB * kMaxR))) != RETOPK_OK ||

@@ -71,7 +71,8 @@ struct Ws {
     int32_t *supp;        // [BH, C, K], ascending, -1 padded
     int32_t *cnt;         // [BH, C]
     // per-step workspaces
-    double *rho_bmax;     // [BH, kMaxCache / kSimSlots] per-k_sim-block maxima of rho
+    uint8_t *reuse;       // [BH] 1: head bh reuses this step (its rho_max >= tau), set by k_sim,
+                          // read by k_score, cleared by k_filter
     int32_t *topr;        // [BH, kMaxCache / kSimSlots, kMaxR] per-k_sim-block Top-R slots
     double *topr_rho;     // [BH, kMaxCache / kSimSlots, kMaxR] their similarities
     int32_t *topr_cnt;    // [BH, kMaxCache / kSimSlots, kMaxR] their support sizes

@@ -466,10 +466,10 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
             w.topr[base + cnt] = slot;
             w.topr_rho[base + cnt] = ri;
             w.topr_cnt[base + cnt] = scnt;
-            if (cnt == 0 && !recent) w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = ri;
+            // the head reuses (Eq. 13) iff some block's best similarity is >= tau
+            // (every such block stores the same flag)
+            if (cnt == 0 && !recent && ri >= (double)a.tau) w.reuse[bh] = 1;
         }
-        if (tid == 0 && sb * kSimSlots >= n_valid && !recent)
-            w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = -INFINITY;
     }
     if (recent && wave == 0) {
         // one lane per slot of the block; list positions past this block's
@@ -486,7 +486,7 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
             w.topr_rho[base + lane] = -INFINITY;
             w.topr_cnt[base + lane] = 0;
         }
-        if (lane == 0) w.rho_bmax[(int64_t)bh * (kMaxCache / kSimSlots) + sb] = m;
+        if (lane == 0 && m >= (double)a.tau) w.reuse[bh] = 1;
     }
 }
 
@@ -798,13 +798,12 @@ __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, 
         __shared__ uint32_t s_local[kLocalGroups];   // group * 256 + exact-head mask
         __shared__ uint32_t s_red[NT / 64];
         const int BH = a.B * a.Hq;
-        for (int i = tid; i < (BH + 31) / 32; i += NT) s_reuse[i] = 0u;
-        __syncthreads();
-        const int nsb = (a.M + kSimSlots - 1) / kSimSlots;
-        for (int t = tid; t < BH * nsb; t += NT) {
-            const int head = t / nsb, sb = t - head * nsb;
-            if (w.rho_bmax[(int64_t)head * (kMaxCache / kSimSlots) + sb] >= (double)a.tau)
-                atomicOr(&s_reuse[head >> 5], 1u << (head & 31));
+        for (int i0 = 0; i0 < BH; i0 += NT) {
+            const uint64_t bal = __ballot(i0 + tid < BH && w.reuse[i0 + tid] != 0);
+            if ((tid & 63) == 0 && i0 + tid < BH) {
+                s_reuse[(i0 + tid) >> 5] = (uint32_t)bal;
+                if (i0 + tid + 32 < BH) s_reuse[((i0 + tid) >> 5) + 1] = (uint32_t)(bal >> 32);
+            }
         }
         __syncthreads();
         auto mask_of = [&](int gi) {
@@ -951,20 +950,14 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
         for (int v = 0; v < R::kNV; ++v) qv[v] = qr[v * 4 + p];
     }
     // In a scan-fed step: whether the head's KV group is scanned (some head of the
-    // group has every block maximum of rho below tau: it falls back), by the rule
-    // the scan blocks apply; bit j of s_grp: head j of the group reuses.
+    // group falls back: its reuse bit is clear), by the rule the scan blocks
+    // apply; bit j of s_grp: head j of the group reuses.
     __shared__ uint32_t s_grp;
-    if (a.scan_fed && wave == 0) {
-        const int64_t head0 = (int64_t)b * a.Hq + (int64_t)g * a.G;
-        uint32_t bits = 0u;
-        for (int i = lane; i < a.G * nsb; i += 64) {
-            const int j = i / nsb, sb = i - j * nsb;
-            if (w.rho_bmax[(head0 + j) * (kMaxCache / kSimSlots) + sb] >= (double)a.tau) bits |= 1u << j;
-        }
+    if (a.scan_fed && tid == 0) {
+        const int head0 = b * a.Hq + g * a.G;
         uint32_t all = 0u;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) all |= __ballot(((bits >> j) & 1u) != 0u) ? 1u << j : 0u;
-        if (lane == 0) s_grp = all;
+        for (int j = 0; j < a.G; ++j) all |= (w.reuse[head0 + j] != 0 ? 1u : 0u) << j;
+        s_grp = all;
     }
     __syncthreads();
 
@@ -1177,6 +1170,10 @@ __global__ __launch_bounds__(kScoreThreads) void k_filter(StepArgs a, Ws w, Geom
     __shared__ uint32_t s_red[NT / 64];
     __shared__ uint32_t s_bstar;
     const int tid = threadIdx.x;
+    // the reuse flags k_sim set for this step were read by k_score; cleared here
+    // for the next step
+    if (a.mode == MODE_SELECT && blockIdx.x == 0)
+        for (int i = tid; i < a.B * a.Hq; i += NT) w.reuse[i] = 0;
     // the filter blocks of (virtual) head vh run on XCD vh % 8 (block j is placed
     // on XCD j % 8), where the head's range blocks wrote its path and candidates
     // and its final blocks read the survivors
