@@ -1493,7 +1493,7 @@ constexpr int kFastRegions = 64;                       // regions one wave ranks
 
 struct FastSmem {
     uint32_t hist[kFastBins];
-    uint64_t tie[kTieMax];
+    uint64_t tie[kTieMax + 64];     // the final bin's entries, then one spare slot a lane
     uint32_t wmax[kFinalThreads / 64], wmin[kFinalThreads / 64];
     uint32_t wsel[kFinalThreads / 64];
     uint32_t n_tie;
@@ -1740,12 +1740,12 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
             wave_find_bin<kFastBins>(fs.hist, k_rem, bstar, above, cnt_b);
             uint32_t in_b = 0u;
             if (wlive) {
+                // branch-free: masks by selects
 #pragma unroll
                 for (int u = 0; u < EPT; ++u) {
-                    if ((cand >> u) & 1u) {
-                        if (bin[u] > bstar) above_mask |= 1u << u;
-                        else if (bin[u] == bstar) in_b |= 1u << u;
-                    }
+                    const uint32_t bit = cand & (1u << u);
+                    above_mask |= bin[u] > bstar ? bit : 0u;
+                    in_b |= bin[u] == bstar ? bit : 0u;
                 }
             }
             cand = in_b;
@@ -1760,33 +1760,46 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
             __syncthreads();
         }
         if (cnt_b > (uint32_t)kTieMax) return false;
-        // the final bin's entries to LDS: one slot reservation per thread
-        if (wlive && cand != 0u) {
-            uint32_t at = atomicAdd(&fs.n_tie, (uint32_t)__popc(cand));
+        // the final bin's entries to LDS: a wave's slots from a prefix sum of its
+        // lanes' counts and one reservation; entries outside the bin go to the
+        // lane's spare slot, so that the writes need no branches
+        if (wlive) {
+            const uint32_t mine = (uint32_t)__popc(cand);
+            const uint32_t inc = wave_incl_scan(mine);
+            const uint32_t wtot = (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+            uint32_t wbase = 0u;
+            if (wtot != 0u) {
+                if (lane == 63) wbase = atomicAdd(&fs.n_tie, wtot);
+                wbase = (uint32_t)__builtin_amdgcn_readlane((int)wbase, 63);
+            }
+            uint32_t at = wbase + inc - mine;
 #pragma unroll
-            for (int u = 0; u < EPT; ++u)
-                if ((cand >> u) & 1u) fs.tie[at++] = e[u];
+            for (int u = 0; u < EPT; ++u) {
+                const bool in = ((cand >> u) & 1u) != 0u;
+                fs.tie[in ? at : (uint32_t)(kTieMax + lane)] = e[u];
+                at += in ? 1u : 0u;
+            }
         }
         __syncthreads();                                              // barrier 3
-        // every wave ranks the bin's entries (lane i holds entry i, the others are
-        // read as scalars): the k_rem-th largest is the threshold
-        const uint64_t x = lane < (int)cnt_b ? fs.tie[lane] : 0ull;
-        const uint32_t xlo = (uint32_t)x, xhi = (uint32_t)(x >> 32);
-        uint32_t higher = 0u;
-        for (int i = 0; i < (int)cnt_b; ++i) {
-            const uint32_t ylo = (uint32_t)__builtin_amdgcn_readlane((int)xlo, i);
-            const uint32_t yhi = (uint32_t)__builtin_amdgcn_readlane((int)xhi, i);
-            higher += (yhi > xhi || (yhi == xhi && ylo > xlo)) ? 1u : 0u;
-        }
-        const uint64_t at = __ballot(lane < (int)cnt_b && higher == k_rem - 1u);
-        const int tl = __builtin_ctzll(at);
-        thr = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)xhi, tl) << 32) |
-              (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)xlo, tl);
-        // selected: every entry above the final bin, and those of it at or above thr
+        // every wave that holds entries ranks the bin's entries (lane i holds entry
+        // i, the others are read as scalars): the k_rem-th largest is the threshold;
+        // selected are every entry above the final bin and those of it at or above
+        // the threshold
         if (wlive) {
+            const uint64_t x = lane < (int)cnt_b ? fs.tie[lane] : 0ull;
+            const uint32_t xlo = (uint32_t)x, xhi = (uint32_t)(x >> 32);
+            uint32_t higher = 0u;
+            for (int i = 0; i < (int)cnt_b; ++i) {
+                const uint32_t ylo = (uint32_t)__builtin_amdgcn_readlane((int)xlo, i);
+                const uint32_t yhi = (uint32_t)__builtin_amdgcn_readlane((int)xhi, i);
+                higher += (yhi > xhi || (yhi == xhi && ylo > xlo)) ? 1u : 0u;
+            }
+            const uint64_t at = __ballot(lane < (int)cnt_b && higher == k_rem - 1u);
+            const int tl = __builtin_ctzll(at);
+            thr = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)xhi, tl) << 32) |
+                  (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)xlo, tl);
 #pragma unroll
-            for (int u = 0; u < EPT; ++u)
-                if (((cand >> u) & 1u) && e[u] >= thr) above_mask |= 1u << u;
+            for (int u = 0; u < EPT; ++u) above_mask |= (cand & (1u << u)) && e[u] >= thr ? 1u << u : 0u;
         }
         valid = above_mask;
     }
