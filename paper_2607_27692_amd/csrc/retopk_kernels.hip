@@ -237,12 +237,15 @@ template <typename T, int D> struct RowT {
 };
 
 // Waves per SIMD that k_score is built for: 4 (two 512-thread blocks per CU), or
-// 2 (256 registers a lane) where the group's query vectors alone would take half
-// of 128 registers (G * kNV * 4 in the quad layout, half that in the octet one of
-// the fp32 8-head build; the bf16 8-head build holds D / 32 MFMA operands).
+// 2 (256 registers a lane) where the group's query vectors and the two key rows a
+// lane holds in flight would take more than 96 of 128 registers (G + 2 rows of
+// kNV * 4 in the quad layout), or, in the octet layout of the fp32 8-head build,
+// where the query vectors alone would take half of them (the bf16 8-head build
+// holds D / 32 MFMA operands).
 template <typename T, int D, int G>
 constexpr int kGroupWaves = (G == 8 && sizeof(T) == 2) ? 4
-                            : ((G == 8 ? 2 : 4) * G * RowT<T, D>::kNV > 64 ? 2 : 4);
+                            : G == 8 ? (2 * G * RowT<T, D>::kNV > 64 ? 2 : 4)
+                                     : ((G + 2) * RowT<T, D>::kNV * 4 > 96 ? 2 : 4);
 // The same for k_dense, whose lanes also hold G value accumulators of kEPV floats
 // (the 8-head build takes its scores in the octet layout, its queries dead by
 // the time the accumulators live).
@@ -1110,8 +1113,9 @@ __device__ void range_block(const StepArgs &a, const Ws &w, int cb, unsigned cha
                 for (int i = tid; i < nr; i += NT) ents[total + rb + i] = (uint64_t)(uint32_t)list[i];
             }
             // Eq. 10 on this round: 4 lanes per key row, four rows per lane in
-            // flight, loaded from clamped (in-bounds) list positions.
-            constexpr int GU = 4;
+            // flight (two for 512-byte rows, whose four would fill the registers),
+            // loaded from clamped (in-bounds) list positions.
+            constexpr int GU = R::kNV >= 8 ? 2 : 4;
             for (int base = 0; !from_scan && base < nr; base += GU * kScanRowsPerIter) {
                 uint4 kv[GU][R::kNV];
                 int ci[GU], cidx[GU];
