@@ -1563,6 +1563,13 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
     const bool sel_mode = a.mode == MODE_SELECT;
     const int64_t len = a.len;
     const int nreg_x = (int)((len + kFilterRows - 1) / kFilterRows);   // exact layout
+    // which of the head's closing writes this block owns (shared out over its slices)
+    const bool own_sel = slice == 0, own_supp = (1 % NS) == slice;
+    const bool own_qbar = (2 % NS) == slice, own_misc = (3 % NS) == slice;
+    // the normalised query k_sim stored, for the cache entry: loaded with the first
+    // round trip so that the closing writes wait for no load
+    static_assert(D <= NT, "one element per thread");
+    const float qcur = a.do_insert && own_qbar && sel_mode && tid < D ? w.qbar_cur[(int64_t)bh * D + tid] : 0.0f;
 
     for (int i = tid; i < kFastBins; i += NT) fs.hist[i] = 0u;
     if (tid == 0) fs.n_tie = 0u;
@@ -1807,6 +1814,19 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
         }
         valid = above_mask;
     }
+    // No early exit from here on: the counters of a reuse head, or the reset of an
+    // exact head's histogram (read by k_filter, the previous launch) for the next
+    // launch, go out now so that their latency overlaps the rest.
+    if (own_misc) {
+        if (reuse) {
+            if (tid == 0) {
+                atomicAdd(&w.stats[STAT_CAND_SUM], (unsigned long long)n);
+                atomicMax(&w.stats[STAT_CAND_MAX], (unsigned long long)n);
+            }
+        } else {
+            for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)bh * kHistBins + i] = 0u;
+        }
+    }
     const uint32_t selm = valid;
     const uint32_t nsel = (uint32_t)__popc(selm);
 
@@ -1878,9 +1898,6 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
         a.out[(int64_t)bh * D + slice * DS + tid] = o / l;
     }
 
-    // which of the head's writes this block owns (shared out over its slices)
-    const bool own_sel = slice == 0, own_supp = (1 % NS) == slice;
-    const bool own_qbar = (2 % NS) == slice, own_misc = (3 % NS) == slice;
     const int64_t ent = (int64_t)bh * a.M + a.insert_slot;   // the cache entry written
     auto put = [&](int32_t *dst) {
         for (int t = tid; t < K; t += NT) dst[t] = t < (int)kn ? (int32_t)(list[t] >> 32) : -1;
@@ -1906,24 +1923,13 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
         }
         if (own_qbar) {
             if (sel_mode) {
-                for (int t = tid; t < D; t += NT) w.qbar[ent * D + t] = w.qbar_cur[(int64_t)bh * D + t];
+                if (tid < D) w.qbar[ent * D + tid] = qcur;
             } else {
                 __shared__ float s_qbar[D];
                 __shared__ double s_red[NT / 64];
                 block_qbar<T, D, NT>((const T *)a.q + (int64_t)bh * a.q_head_stride, s_qbar, s_red);
                 for (int t = tid; t < D; t += NT) w.qbar[ent * D + t] = s_qbar[t];
             }
-        }
-    }
-    if (own_misc) {
-        if (reuse) {
-            if (tid == 0) {
-                atomicAdd(&w.stats[STAT_CAND_SUM], (unsigned long long)n);
-                atomicMax(&w.stats[STAT_CAND_MAX], (unsigned long long)n);
-            }
-        } else {
-            // leave the histogram zeroed for the next launch
-            for (int i = tid; i < kHistBins; i += NT) w.hist[(int64_t)bh * kHistBins + i] = 0u;
         }
     }
     return true;
