@@ -3,7 +3,8 @@
 // One decode step is four launches on the caller's stream, and blocks never wait
 // on each other inside a launch (every hand-over is a kernel boundary):
 //   k_sim     cosine similarity of q_bar to every cached query (Eq. 5, Eq. 6),
-//             64 cache slots per block, plus per-block maxima of rho.
+//             64 cache slots per block: each block's Top-R list, and a per-head
+//             flag set when some block's best similarity reaches tau.
 //   k_score   (a) full-history QK scan of every KV group with an exact head
 //             (Eq. 4): one key-row load serves the G query heads of the group, and
 //             each block adds its scores to a per-head histogram;
@@ -20,7 +21,10 @@
 //             then aggregates one slice of the head dimension of Softmax-V
 //             (Eq. 12); the writes of the support and of the cache entry
 //             (Sec. 3.4) are shared out over the slices.
-// Exact Top-K attention alone is k_score (scan only) + k_filter + k_final.
+// Exact Top-K attention alone is the full-history scan (k_scan_list where every
+// CU can own one whole 4096-row filter region, keeping each region's scores in
+// LDS and writing its local survivors; otherwise k_score's scan blocks) +
+// k_filter + k_final.
 // A head's similarity, range and final blocks run on one XCD (blocks are placed
 // on XCDs round-robin by block index), so that blocks sharing a head's data
 // (Top-R lists, supports, value rows) share that XCD's L2.
@@ -428,8 +432,9 @@ __global__ __launch_bounds__(kSimThreads) void k_sim(StepArgs a, Ws w)
     // compare slot `local` against 16 slots each; rank = number of slots that are
     // more similar, or equally similar and newer (with recent-R retrieval: that
     // are newer).  The global Top-R is contained in the union of the blocks'
-    // lists.  The block's maximum of rho over the entries retrieval can use goes
-    // to rho_bmax: every valid slot for Eq. 7, the R most recent for recent-R.
+    // lists.  The head's reuse flag is set when the block's best similarity over
+    // the entries retrieval can use reaches tau: every valid slot for Eq. 7, the R
+    // most recent for recent-R.
     const bool recent = a.retrieval == 1;
     {
         const double ri = s_rho[local];
@@ -761,7 +766,8 @@ __device__ void scan_segment(const StepArgs &a, const Ws &w, int b, int g, uint3
 // Scan block sbk: scores its share of the concatenated rows of the KV groups that
 // have an exact head, so that the scan work spreads over all scan blocks however
 // many groups need it.  Outside MODE_SELECT every group is exact; in MODE_SELECT
-// a head is exact iff rho_max < tau (Eq. 13), read from the k_sim block maxima.
+// a head is exact iff rho_max < tau (Eq. 13): its reuse flag, which k_sim sets
+// when some block's best similarity reaches tau, is clear.
 template <typename T, int D, int G, bool kSelect>
 __device__ void scan_block(const StepArgs &a, const Ws &w, const Geometry &geo, int sbk,
                            unsigned char *lds)
