@@ -1673,11 +1673,14 @@ __device__ bool final_fast(const StepArgs &a, const Ws &w, int bh, int slice, Fa
             const uint32_t st = (uint32_t)__shfl((int)(tincl - need), c < 64 ? c : 63);
             if (c < nreg && st <= (uint32_t)tid) lo = c;
         }
+        // the shuffles read lane lo, so every lane takes part (a lane outside the
+        // branch below may be the one read)
         const uint32_t st0 = (uint32_t)__shfl((int)(tincl - need), lo);
         const uint32_t rc = (uint32_t)__shfl((int)rcnt, lo);
+        const uint32_t rpos = (uint32_t)__shfl((int)(incl - rcnt), lo);
         const uint32_t j0 = ((uint32_t)tid - st0) * EPT;
         if ((uint32_t)tid < tall && j0 < rc) {
-            p0 = (uint32_t)__shfl((int)(incl - rcnt), lo) + j0;
+            p0 = rpos + j0;
             nlive = rc - j0 < (uint32_t)EPT ? rc - j0 : (uint32_t)EPT;
             const uint64_t *src = base + (int64_t)lo * stride + j0;
             if ((stride & 1) == 0) {

@@ -177,6 +177,13 @@ SHAPES = [
                             n_centers=12)),
     ("f32_d64_g5", dict(dtype="f32", n_q_heads=10, n_kv_heads=2, head_dim=64, prompt_len=2500,
                         steps=32, k=48, cache_cap=24, r=4, window=32, refresh=12, n_centers=12)),
+    # candidate sets smaller than one thread's share of the final stage (R K + W < 8):
+    # most index ranges are empty and few threads hold entries
+    ("f32_cap7", dict(dtype="f32", n_q_heads=4, n_kv_heads=2, head_dim=64, prompt_len=3000,
+                      steps=16, k=7, cache_cap=5, r=1, window=0, refresh=5, n_centers=7,
+                      p_jump=0.3)),
+    ("bf16_k1", dict(n_q_heads=6, n_kv_heads=2, head_dim=64, prompt_len=3000, steps=16, k=1,
+                     cache_cap=5, r=3, window=1, refresh=0, tau=0.5, n_centers=6)),
 ]
 
 
