@@ -1,0 +1,98 @@
+"""GPU parity on seeded random configurations: combinations of shape, dtype, group
+size, K, cache capacity, R, window, tau, refresh period, retrieval rule and input
+distribution that the hand-picked cases do not pair up, small enough for the
+oracle to finish each in well under a second.
+
+* decode steps in lock-step with the oracle (Sec. 3.3-3.4; the rules of
+  test_gpu_decode: path, rho_max, retrieved slots, candidates, support, output,
+  inserted cache entry);
+* exact_topk_attention (Eq. 1, Eq. 4, Eq. 12; the rules of test_gpu_exact);
+* the prefill initialisation's cache state (Sec. 3.3; the rules of
+  test_gpu_prefill).
+
+Every configuration is drawn from a fixed seed, so a failure names a
+reproducible case."""
+import numpy as np
+import pytest
+
+import test_gpu_decode as TD
+import test_gpu_exact as TE
+import test_gpu_prefill as TP
+from gpu_harness import Tally, params_of
+from oracle import oracle as O
+from paper_2607_27692_amd.inputs import WORKLOADS, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _decode_cfg(i):
+    rng = np.random.default_rng(1000 + i)
+    G = int(rng.choice([1, 2, 3, 4, 5, 7, 8]))
+    Hkv = int(rng.integers(1, 3))
+    M = int(rng.choice([1, 2, 5, 16, 33, 64, 100]))
+    K = int(rng.choice([1, 7, 64, 100, 256, 513, 1024]))
+    change = dict(batch=int(rng.integers(1, 3)), n_q_heads=G * Hkv, n_kv_heads=Hkv,
+                  head_dim=int(rng.choice([64, 128])), dtype=str(rng.choice(["bf16", "f32"])),
+                  prompt_len=int(rng.integers(max(64, K // 2), 9000)),
+                  steps=int(rng.integers(6, 12)), k=K, cache_cap=M,
+                  r=int(rng.integers(1, min(32, M) + 1)),
+                  window=int(rng.choice([0, 1, 17, 64, 256])),
+                  tau=float(rng.choice([-1.0, 0.5, 0.8, 0.9, 0.97, 2.0])),
+                  refresh=int(rng.choice([0, 3, 5, 16])),
+                  p_jump=float(rng.choice([0.0, 0.05, 0.3])),
+                  n_centers=int(rng.integers(2, 24)), seed=int(rng.integers(1 << 30)))
+    return change, int(rng.choice([0, 0, 0, 1]))
+
+
+@pytest.mark.parametrize("i", range(40))
+def test_decode_random(i):
+    change, retrieval = _decode_cfg(i)
+    w = WORKLOADS["16k"].with_(name=f"random{i}", **change)
+    print(f"decode random {i}: {change} retrieval={retrieval}", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w, retrieval=retrieval)
+    heads = list(range(p.heads))
+    tally, _ = TD._lockstep(w, inp, p, heads, w.steps)
+    print(tally, flush=True)
+    assert tally.exact + tally.near_tie + tally.path_tie + tally.rho_tie == len(heads) * w.steps
+
+
+def _exact_cfg(i):
+    rng = np.random.default_rng(2000 + i)
+    G = int(rng.choice([1, 2, 3, 4, 5, 6, 7, 8]))
+    Hkv = int(rng.integers(1, 4))
+    L = int(rng.choice([1, 2, 7, 100, 4095, 4096, 4097, int(rng.integers(1, 40000))]))
+    kind = str(rng.choice(["randn", "randn", "ties", "negative", "equal"]))
+    if kind == "ties" and L < 3:   # the ties recipe draws from 3 key rows
+        kind = "randn"
+    return (str(rng.choice(["bf16", "f32"])), int(rng.choice([64, 128])), int(rng.integers(1, 3)),
+            G * Hkv, Hkv, L, int(rng.choice([1, 2, 31, 64, 100, 511, 512, 1000, 2048])), kind)
+
+
+@pytest.mark.parametrize("i", range(30))
+def test_exact_random(i):
+    TE.test_exact_parity(*_exact_cfg(i))
+
+
+@pytest.mark.parametrize("i", range(20))
+def test_prefill_random(i):
+    rng = np.random.default_rng(3000 + i)
+    G = int(rng.choice([1, 2, 3, 4, 5, 7, 8]))
+    Hkv = int(rng.integers(1, 3))
+    C = int(rng.choice([1, 3, 16, 40, 77, 130]))
+    change = dict(batch=int(rng.integers(1, 3)), n_q_heads=G * Hkv, n_kv_heads=Hkv,
+                  head_dim=int(rng.choice([64, 128])), dtype=str(rng.choice(["bf16", "bf16", "f32"])),
+                  k=int(rng.choice([1, 7, 64, 200, 513, 2048])), cache_cap=C,
+                  prompt_len=int(rng.integers(max(2, C), 12000)), steps=1, r=1, window=0,
+                  n_centers=int(rng.integers(2, 20)), seed=int(rng.integers(1 << 30)))
+    w = WORKLOADS["16k"].with_(name=f"prefill_random{i}", **change)
+    print(f"prefill random {i}: {change}", flush=True)
+    inp = make_inputs(w)
+    p = params_of(w)
+    orc = O.Oracle(p)
+    orc.prefill_init(inp.q_tail, inp.k, inp.v, w.prompt_len)
+    gst = TP._gpu_prefill(p, w.dtype, inp.q_tail_raw, inp.k_raw, inp.v_raw, w.prompt_len)
+    tally = Tally()
+    TP._compare_states(p, gst, orc.get_state(), list(range(p.heads)), inp.q_tail, inp.k,
+                       w.prompt_len, tally)
+    print(tally, flush=True)
