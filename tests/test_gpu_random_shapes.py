@@ -8,7 +8,10 @@ oracle to finish each in well under a second.
   inserted cache entry);
 * exact_topk_attention (Eq. 1, Eq. 4, Eq. 12; the rules of test_gpu_exact);
 * the prefill initialisation's cache state (Sec. 3.3; the rules of
-  test_gpu_prefill).
+  test_gpu_prefill);
+* free-running trajectories: the GPU's own prefill and cache evolution over 20-70
+  steps against the oracle's own, head by head up to a near-tie (the rules of
+  test_gpu_decode).
 
 Every configuration is drawn from a fixed seed, so a failure names a
 reproducible case."""
@@ -96,3 +99,28 @@ def test_prefill_random(i):
     TP._compare_states(p, gst, orc.get_state(), list(range(p.heads)), inp.q_tail, inp.k,
                        w.prompt_len, tally)
     print(tally, flush=True)
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_free_running_random(i):
+    rng = np.random.default_rng(4000 + i)
+    G = int(rng.choice([1, 2, 4, 7, 8]))
+    Hkv = int(rng.integers(1, 3))
+    M = int(rng.choice([3, 8, 16, 33]))
+    K = int(rng.choice([1, 16, 64, 256]))
+    change = dict(batch=int(rng.integers(1, 3)), n_q_heads=G * Hkv, n_kv_heads=Hkv,
+                  head_dim=int(rng.choice([64, 128])), dtype=str(rng.choice(["bf16", "f32"])),
+                  prompt_len=int(rng.integers(max(M + 1, K), 8000)),
+                  steps=int(rng.integers(20, 70)), k=K, cache_cap=M,
+                  r=int(rng.integers(1, M + 1)), window=int(rng.choice([0, 16, 64])),
+                  tau=float(rng.choice([0.5, 0.8, 0.9])), refresh=int(rng.choice([0, 7, 16])),
+                  p_jump=float(rng.choice([0.0, 0.05, 0.2])),
+                  n_centers=int(rng.integers(3, 20)), seed=int(rng.integers(1 << 30)))
+    w = WORKLOADS["16k"].with_(name=f"free_random{i}", **change)
+    print(f"free-running random {i}: {change}", flush=True)
+    inp = make_inputs(w)
+    run = TD._free_run(w, inp, TD._dev_inputs(inp), w.steps)
+    heads = list(range(w.batch * w.n_q_heads))
+    compared, parted = TD._follow(w, inp, run, heads, w.steps)
+    print(f"compared {compared} of {len(heads) * w.steps} head-steps, parted {parted}", flush=True)
+    assert compared >= 0.5 * len(heads) * w.steps
